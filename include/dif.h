@@ -1,0 +1,252 @@
+/*
+ * dif.h - C ABI of the step-pruned video-DiT denoise step on MI355X (gfx950).
+ *
+ * Problem (Sec. 3.1, Sec. 3.2, Sec. 4.3 of "Dynamic-in-Few-Step"): a T = 4
+ * step few-step sampler visits timesteps t_1 (most noise) .. t_4.  Step t_i
+ * runs its own structure: binary gates g_{t_i} keep or remove whole blocks,
+ * attention heads and FFN hidden channels, and a gate multiplies the output
+ * of the component it controls (gating equation, Sec. 3.2).  The trained
+ * network is exported to one dense network per step (Sec. 3.2), and the
+ * inference engine keeps the union of all steps' parameters plus per-step
+ * index tables, gathering each step's active parameters (Sec. 4.3).  Given
+ * latent video tokens z_t, the timestep t, the text context c and the step
+ * structure, one denoise step returns the model prediction v_t (Sec. 4.2
+ * "predicted clean data ... computed from the model prediction v_t").
+ *
+ * Block internals are not given by the paper (it names a Wan2.1 DiT,
+ * Sec. 5.1).  The library implements a Wan2.1-style block:
+ *   x += gate1 * (SelfAttn(RoPE(RMSNorm_D(q)), RoPE(RMSNorm_D(k)), v) Wo^T + bo)
+ *        with q,k,v projected from LN(x) * (1 + scale1) + shift1
+ *   x += CrossAttn(RMSNorm_D(q_c), RMSNorm_D(k_c), v_c) Wco^T + bco
+ *        with q_c from LN_affine(x), k_c, v_c from the text context
+ *   x += gate2 * (GELU_tanh(LN(x)(1 + scale2) + shift2) W1^T + b1) W2^T + b2)
+ * where (shift1, scale1, gate1, shift2, scale2, gate2) = layer modulation +
+ * e0(t), RMSNorm_D spans the full width D with pruned channels counted as
+ * zeros, and a pruned head / channel contributes nothing.
+ *
+ * Conventions
+ *   - Every call returns dif_status: 0 on success, a negative DIF_E_* code
+ *     on error.  No C++ exception and no abort ever crosses this ABI.  After
+ *     an error, dif_last_error() returns a thread-local description.
+ *   - Device pointers are HIP device addresses owned by the caller (the
+ *     library never frees them).  Host pointers are read during the call
+ *     only, unless stated.  The library allocates no device memory: plan
+ *     memory and workspaces are caller-provided, sized by the *_bytes calls.
+ *   - Kernel launches are asynchronous on the caller's hipStream_t (NULL =
+ *     the default stream).  A fault inside a kernel surfaces at the caller's
+ *     next synchronisation, or as DIF_E_HIP from a later call.
+ *   - Matrices are row-major, nn.Linear layout [out_features, in_features].
+ *     "dtype" storage is bfloat16 (DIF_BF16) or float32 (DIF_F32); norm,
+ *     bias, gain and modulation vectors are always float32.
+ *   - Calls on one model/plan from several host threads must be serialised
+ *     by the caller; distinct plans may be used concurrently on distinct
+ *     streams with distinct workspaces.
+ */
+#ifndef DIF_H_
+#define DIF_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t dif_status;
+#define DIF_OK 0
+#define DIF_E_ARG (-1)          /* null pointer, bad enum, bad scalar       */
+#define DIF_E_SHAPE (-2)        /* inconsistent or unsupported sizes        */
+#define DIF_E_MASK (-3)         /* mask entry not 0/1, or wrong length      */
+#define DIF_E_UNSUPPORTED (-4)  /* (dtype, head_dim) pair or device arch     */
+#define DIF_E_WORKSPACE (-5)    /* plan memory / workspace too small or misaligned */
+#define DIF_E_HIP (-6)          /* a HIP runtime call failed                */
+
+typedef enum { DIF_BF16 = 0, DIF_F32 = 1 } dif_dtype;
+
+/* Model hyper-parameters.  Supported (dtype, head_dim): (BF16,128), (F32,64),
+ * (F32,128).  dim == n_heads * head_dim; dim % 64 == 0; dim <= 8192 (BF16)
+ * or 4096 (F32); patch_dim % 64 == 0; freq_dim even; grid_* >= 1. */
+typedef struct dif_config {
+  int32_t dim;          /* D  */
+  int32_t n_heads;      /* H  */
+  int32_t head_dim;     /* dh */
+  int32_t ffn_dim;      /* F  */
+  int32_t n_layers;     /* N  */
+  int32_t patch_dim;    /* Cp: latent features per token */
+  int32_t freq_dim;     /* sinusoidal timestep features (256) */
+  int32_t grid_f, grid_h, grid_w; /* latent token grid; L = f*h*w */
+  int32_t max_text_len; /* upper bound on Lc accepted by the calls */
+  int32_t dtype;        /* dif_dtype */
+  float eps;            /* LayerNorm / RMSNorm epsilon (1e-6) */
+  float rope_theta;     /* RoPE base (10000) */
+} dif_config;
+
+/* One block's parameters (device pointers, caller-owned, must outlive the
+ * model and every plan built from it).  W* are [D, D] dtype unless stated. */
+typedef struct dif_layer_weights {
+  const float* mod;                     /* [6, D]: shift1 scale1 gate1 shift2 scale2 gate2 */
+  const void* self_wq; const void* self_wk; const void* self_wv; const void* self_wo;
+  const float* self_bq; const float* self_bk; const float* self_bv; const float* self_bo; /* [D] */
+  const float* self_gq; const float* self_gk;   /* RMSNorm gains [D] */
+  const float* norm3_w; const float* norm3_b;   /* cross-attention LayerNorm affine [D] */
+  const void* cross_wq; const void* cross_wk; const void* cross_wv; const void* cross_wo;
+  const float* cross_bq; const float* cross_bk; const float* cross_bv; const float* cross_bo;
+  const float* cross_gq; const float* cross_gk;
+  const void* ffn_w1;   /* [F, D] */
+  const float* ffn_b1;  /* [F]    */
+  const void* ffn_w2;   /* [D, F] */
+  const float* ffn_b2;  /* [D]    */
+} dif_layer_weights;
+
+/* The union-of-all-steps parameter set theta_union (Sec. 4.3). */
+typedef struct dif_weights {
+  const void* patch_w;  const float* patch_b;  /* [D, Cp], [D]           */
+  const void* t_w1;     const float* t_b1;     /* [D, freq_dim], [D]     */
+  const void* t_w2;     const float* t_b2;     /* [D, D], [D]            */
+  const void* t_w3;     const float* t_b3;     /* [6D, D], [6D]          */
+  const float* head_mod;                       /* [2, D]: shift, scale   */
+  const void* head_w;   const float* head_b;   /* [Cp, D], [Cp]          */
+  const dif_layer_weights* layers;             /* host array [n_layers], copied */
+} dif_weights;
+
+/* One step's structure g_t (Sec. 3.2: gate tensors [T, N_block], [T, N_head],
+ * [T, N_channel], here one step's slice per layer).  Host memory, entries 0
+ * or 1.  Self- and cross-attention heads are gated independently. */
+typedef struct dif_step_masks {
+  const uint8_t* block_keep;      /* [n_layers]            */
+  const uint8_t* self_head_keep;  /* [n_layers * n_heads]  */
+  const uint8_t* cross_head_keep; /* [n_layers * n_heads]  */
+  const uint8_t* ffn_keep;        /* [n_layers * ffn_dim]  */
+} dif_step_masks;
+
+/* Kept widths of one layer in a plan (for FLOP accounting and tests). */
+typedef struct dif_layer_info {
+  int32_t block_keep;
+  int32_t self_heads;   /* h   */
+  int32_t cross_heads;  /* h_c */
+  int32_t ffn_channels; /* f   */
+  int32_t ffn_padded;   /* f rounded up to 64: width of the compacted FFN */
+} dif_layer_info;
+
+typedef struct dif_model dif_model;
+typedef struct dif_plan dif_plan;
+typedef struct ihipStream_t* dif_stream; /* == hipStream_t */
+
+/* Description of the last error on the calling thread ("" if none). */
+const char* dif_last_error(void);
+
+/* Host-only validation (no HIP call): DIF_OK, DIF_E_ARG, DIF_E_SHAPE or
+ * DIF_E_UNSUPPORTED for the config; DIF_E_MASK for masks. */
+dif_status dif_validate_config(const dif_config* cfg);
+dif_status dif_validate_masks(const dif_config* cfg, const dif_step_masks* masks);
+
+/* Record the model: validates cfg and that every weight pointer is non-null,
+ * copies the layer array, checks the current device is gfx950 (else
+ * DIF_E_UNSUPPORTED).  No device memory is allocated or copied. */
+dif_status dif_model_create(const dif_config* cfg, const dif_weights* w, dif_model** out);
+dif_status dif_model_destroy(dif_model* model);
+
+/* Bytes of device plan memory dif_plan_step needs for these masks. */
+dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, size_t* bytes);
+
+/* Build the per-step index tables I_t and gather step t's active parameters
+ * into contiguous per-layer weights (Sec. 4.3; the "dense format" of
+ * Sec. 3.2): kept q/k/v rows concatenated as one [3a, D] matrix, kept Wo
+ * columns [D, a], the same for cross-attention, kept W1 rows / b1 entries
+ * and W2 columns zero-padded to a multiple of 64 channels.  Kept indices
+ * are in ascending order.  `step` is the structure's index in the sampler
+ * (0-based, < 4096), kept for the caller's bookkeeping.  plan_mem: caller
+ * device memory of >= dif_plan_bytes bytes, 256-byte aligned, which must
+ * stay valid until dif_plan_destroy.  The gather kernels and a small table
+ * upload are enqueued on `stream`; the host index tables are owned by the
+ * plan.  Errors: DIF_E_MASK, DIF_E_WORKSPACE (too small / misaligned),
+ * DIF_E_HIP. */
+dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_masks* masks,
+                         void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out);
+/* Frees the plan's host metadata only (plan_mem stays the caller's).  The
+ * caller must synchronise `stream` before freeing plan_mem. */
+dif_status dif_plan_destroy(dif_plan* plan);
+dif_status dif_plan_layer_info(const dif_plan* plan, int32_t layer, dif_layer_info* out);
+
+/* Bytes of device workspace dif_block_forward / dif_step_forward need for
+ * B samples of L video tokens and Lc text tokens. */
+dif_status dif_workspace_bytes(const dif_model* model, int32_t B, int32_t L, int32_t Lc,
+                               size_t* bytes);
+
+/* Timestep embedding: e [D] and e0 [6, D] (float32 device outputs) for
+ * timestep t.  Uses the workspace's scratch. */
+dif_status dif_time_embed(const dif_model* model, float t, float* e_out, float* e0_out,
+                          void* ws, size_t ws_bytes, dif_stream stream);
+
+/* One block (layer `layer`) of the plan's step structure, in place on the
+ * residual stream x [B, L, D] (dtype).  ctx [B, Lc, D] (dtype) text tokens,
+ * e0 [6, D] float32 step modulation (B samples share the step, Sec. 2.2:
+ * routing that depends only on the step allows plain batching).  L must
+ * equal grid_f*grid_h*grid_w (the RoPE grid); 1 <= Lc <= max_text_len.
+ * A block whose gate is 0 leaves x unchanged and launches nothing. */
+dif_status dif_block_forward(const dif_plan* plan, int32_t layer, void* x, const void* ctx,
+                             const float* e0, int32_t B, int32_t L, int32_t Lc,
+                             void* ws, size_t ws_bytes, dif_stream stream);
+
+/* One denoise step: model prediction v [B, L, Cp] (float32) for latents
+ * z [B, L, Cp] (float32) at timestep t under the plan's structure:
+ * timestep embedding, patch embedding, the N blocks, output head. */
+dif_status dif_step_forward(const dif_plan* plan, const float* z, float t, const void* ctx,
+                            int32_t B, int32_t L, int32_t Lc, float* v_out,
+                            void* ws, size_t ws_bytes, dif_stream stream);
+
+/* Euler update between sampler steps, in place: z += (sigma_to - sigma_from) * v,
+ * n float32 elements. */
+dif_status dif_euler(float* z, const float* v, float sigma_from, float sigma_to, int64_t n,
+                     dif_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Operator-level entry points: the hot kernels on their own, for tests and
+ * benchmarks of a single kernel.
+ * ---------------------------------------------------------------------- */
+
+/* Epilogues of dif_gemm: C = A B^T (+ bias) then
+ *   DIF_EPI_STORE:    C = acc + bias
+ *   DIF_EPI_GELU:     C = GELU_tanh(acc + bias)
+ *   DIF_EPI_RESIDUAL: C += (gate0 + gate1) * (acc + bias), gate* per column
+ *                     (gate0 == NULL: gate 1)  */
+typedef enum { DIF_EPI_STORE = 0, DIF_EPI_GELU = 1, DIF_EPI_RESIDUAL = 2 } dif_epilogue;
+
+/* C[M, N] (out_dtype) = epilogue(A[M, K] B[N, K]^T), A and B in `dtype`,
+ * float32 accumulation.  K % 64 == 0 for BF16, K % 32 == 0 for F32; K may
+ * be 0 (acc = 0).  lda, ldb, ldc in elements, multiples of 16 bytes;
+ * bias [N] float32 or NULL.  out_dtype = dtype or DIF_F32. */
+dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda,
+                    const void* B, int64_t ldb, void* C, int64_t ldc,
+                    int32_t M, int32_t N, int32_t K, int32_t epilogue, const float* bias,
+                    const float* gate0, const float* gate1, dif_stream stream);
+
+/* Flash attention, bidirectional, scale 1/sqrt(head_dim):
+ * O[b, i, h*dh:(h+1)*dh] = softmax_j(Q_bih . K_bjh / sqrt(dh)) V_bjh.
+ * Q: row (b*Lq + i), column h*dh, row stride ldq.  K: row (b*Lk + j),
+ * row stride ldk.  V is given transposed: Vt[(b*n_heads + h)*dh + d][j],
+ * row stride ldvt >= Lk (ldvt a multiple of 16 bytes).  O like Q with
+ * stride ldo.  1 <= Lk; head_dim 128 (BF16) or 64/128 (F32). */
+dif_status dif_attention(int32_t dtype, int32_t head_dim, const void* Q, int64_t ldq,
+                         const void* K, int64_t ldk, const void* Vt, int64_t ldvt,
+                         void* O, int64_t ldo, int32_t B, int32_t Lq, int32_t Lk,
+                         int32_t n_heads, dif_stream stream);
+
+/* ------------------------------------------------------------------------
+ * Kernel timing: while enabled, every kernel the library launches is
+ * bracketed by HIP events on its stream, grouped by kind, with the kind's
+ * algorithmic FLOPs and bytes.  dif_profile_collect synchronises on the
+ * recorded events and returns, per kind, launches / total ms / FLOPs /
+ * bytes.  Kinds are listed by dif_profile_kind_name(i) for i < DIF_PROF_KINDS.
+ * ---------------------------------------------------------------------- */
+#define DIF_PROF_KINDS 16
+dif_status dif_profile_enable(int32_t on);
+dif_status dif_profile_reset(void);
+const char* dif_profile_kind_name(int32_t kind);
+dif_status dif_profile_collect(int64_t* launches, double* total_ms, double* flops,
+                               double* bytes); /* each an array of DIF_PROF_KINDS */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DIF_H_ */

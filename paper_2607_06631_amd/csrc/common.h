@@ -1,0 +1,120 @@
+// Device-side building blocks shared by the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dif {
+
+typedef __bf16 bf16;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+constexpr int kXcds = 8;   // MI355X: 8 XCDs, workgroups dispatched round-robin
+
+__device__ __forceinline__ float to_f32(float x) { return x; }
+__device__ __forceinline__ float to_f32(bf16 x) { return (float)x; }
+
+template <typename T> __device__ __forceinline__ T from_f32(float x);
+template <> __device__ __forceinline__ float from_f32<float>(float x) { return x; }
+template <> __device__ __forceinline__ bf16 from_f32<bf16>(float x) { return (bf16)x; }
+
+// A 16-byte chunk holds VEC elements of T.
+template <typename T> struct Chunk {
+  static constexpr int VEC = 16 / sizeof(T);
+  __device__ static void unpack(const u32x4& c, float* out) {
+    if constexpr (sizeof(T) == 4) {
+      f32x4 v = __builtin_bit_cast(f32x4, c);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) out[e] = v[e];
+    } else {
+      bf16x8 v = __builtin_bit_cast(bf16x8, c);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) out[e] = (float)v[e];
+    }
+  }
+  __device__ static u32x4 pack(const float* in) {
+    if constexpr (sizeof(T) == 4) {
+      f32x4 v;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) v[e] = in[e];
+      return __builtin_bit_cast(u32x4, v);
+    } else {
+      bf16x8 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = (bf16)in[e];
+      return __builtin_bit_cast(u32x4, v);
+    }
+  }
+};
+
+// One MFMA "k-step" on 32x32 tiles: every lane contributes one 16-byte
+// chunk of A (row lane%32) and of B (column lane%32); lane group lane/32
+// covers the second half of the k extent.
+//   bf16: v_mfma_f32_32x32x16_bf16, k extent 16
+//   f32 : 4 x v_mfma_f32_32x32x2_f32, k extent 8 (element e of both groups)
+template <typename T> struct Mma;
+template <> struct Mma<bf16> {
+  static constexpr int KS = 16;
+  __device__ __forceinline__ static void step(f32x16& acc, const u32x4& a, const u32x4& b) {
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                  __builtin_bit_cast(bf16x8, b), acc, 0, 0, 0);
+  }
+};
+template <> struct Mma<float> {
+  static constexpr int KS = 8;
+  __device__ __forceinline__ static void step(f32x16& acc, const u32x4& a, const u32x4& b) {
+    f32x4 fa = __builtin_bit_cast(f32x4, a), fb = __builtin_bit_cast(f32x4, b);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[0], fb[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[1], fb[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[2], fb[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[3], fb[3], acc, 0, 0, 0);
+  }
+};
+
+// Row of accumulator register r for lane group g in a 32x32 MFMA tile
+// (column is lane % 32).
+__device__ __forceinline__ int acc_row(int r, int g) { return 8 * (r >> 2) + 4 * g + (r & 3); }
+
+// Workgroup `bid` runs on XCD bid % 8.  Return a logical tile index such
+// that each XCD receives one contiguous range of logical tiles, so tiles
+// that share operands share that XCD's L2.
+__device__ __forceinline__ int xcd_remap(int bid, int total) {
+  const int q = total / kXcds, r = total % kXcds;
+  const int x = bid % kXcds, local = bid / kXcds;
+  return (x < r) ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
+}
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Sum over a workgroup of `nwaves` waves; every thread gets the total.
+template <int NWAVES>
+__device__ __forceinline__ float block_sum(float v, float* red /* [NWAVES] */) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < NWAVES; ++i) t += red[i];
+  return t;
+}
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;  // sqrt(2/pi)
+  const float u = c * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.f + tanhf(u));
+}
+
+__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
+
+}  // namespace dif

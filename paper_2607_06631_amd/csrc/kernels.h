@@ -1,0 +1,71 @@
+// Host-side launchers of the gfx950 kernels (internal to libdif).
+// Every launcher enqueues on `stream` and returns hipGetLastError().
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dif {
+
+typedef __bf16 bf16;
+
+enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESIDUAL = 2 };
+
+// C[M,N] = epi(A[M,K] * B[N,K]^T); T in {float, __bf16}; OutT in {T, float}.
+template <typename T, typename OutT>
+hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
+                       int M, int N, int K, int epi, const float* bias, const float* gate0,
+                       const float* gate1, hipStream_t stream);
+
+// Flash attention; V given transposed (see dif_attention in dif.h).
+template <typename T>
+hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, int64_t ldk,
+                            const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk,
+                            int H, hipStream_t stream);
+
+// Row LayerNorm of x [M, D] then
+//   mode 0: y = xhat * (1 + p2 + p3) + (p0 + p1)      (AdaLN; p1/p3 may be null)
+//   mode 1: y = xhat * p0 + p1                          (affine)
+template <typename T>
+hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0,
+                       const float* p1, const float* p2, const float* p3, float eps,
+                       hipStream_t stream);
+
+// In place on rows of buf (stride ld): for each of nseg segments of width a
+// at column offset off[s]: y = x / sqrt(sum(x^2) * inv_norm_dim + eps) * gain[s][c],
+// then (rope != null) rotate consecutive pairs of each head_dim-wide head by
+// the token's 3D angles.
+struct RopeDesc {
+  const float* table;  // float2 (cos, sin) entries, see rope_table_size
+  int L;               // tokens per sample (row % L = token)
+  int gf, gh, gw;      // token grid
+  int jt, jh, jw;      // pairs per axis
+  int head_dim;
+};
+template <typename T>
+hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off0, int off1,
+                          const float* g0, const float* g1, float inv_norm_dim, float eps,
+                          const RopeDesc* rope, hipStream_t stream);
+
+// Vt[(b*a + c)*ldvt + j] = src[(b*Lk + j)*lds + c] for j < Lk, 0 for Lk <= j < ldvt.
+template <typename T>
+hipError_t launch_transpose_vt(const T* src, int64_t lds, int a, int B, int Lk, T* Vt,
+                               int64_t ldvt, hipStream_t stream);
+
+// dst[r][c] = src[ridx[r]][cidx[c]] (identity when an index table is null,
+// zero when an index is negative).
+template <typename T>
+hipError_t launch_gather(const T* src, int64_t lds, T* dst, int64_t ldd, int rows, int cols,
+                         const int32_t* ridx, const int32_t* cidx, hipStream_t stream);
+
+// out[n] = act_out(sum_k W[n,k] * x[k] + bias[n]); W [N, K] row-major.
+template <typename T>
+hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out, int N, int K,
+                       hipStream_t stream);
+
+hipError_t launch_sinusoid(float t, int dim, float* out, hipStream_t stream);
+hipError_t launch_silu(const float* x, float* y, int n, hipStream_t stream);
+hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStream_t stream);
+template <typename T>
+hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream);
+
+}  // namespace dif

@@ -1,0 +1,330 @@
+// HBM-bound row kernels for gfx950: LayerNorm + AdaLN modulation,
+// QK RMSNorm + 3D RoPE, V transpose, plan-time gather, timestep GEMV and
+// small elementwise steps.  Rows are read once with 16-byte vector loads,
+// kept in registers between the statistics and the apply pass, and written
+// once; statistics are fp32 whatever the storage type.
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace dif {
+
+constexpr int R_THREADS = 256;
+constexpr int R_WAVES = R_THREADS / kWave;
+constexpr int R_MAXC = 4;  // 16-byte chunks per thread per row
+
+// ---------------------------------------------------------------------------
+// LayerNorm (biased variance, eps) + AdaLN modulation or affine
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void norm_kernel(const T* __restrict__ x, T* __restrict__ y,
+                                                         int D, int mode, const float* p0,
+                                                         const float* p1, const float* p2,
+                                                         const float* p3, float eps) {
+  constexpr int VEC = Chunk<T>::VEC;
+  __shared__ float red[R_WAVES];
+  const int64_t row = blockIdx.x;
+  const int nch = D / VEC;
+  const T* xr = x + row * D;
+  float v[R_MAXC][VEC];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < R_MAXC; ++i) {
+    const int c = threadIdx.x + R_THREADS * i;
+    if (c < nch) {
+      Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(xr + c * VEC), v[i]);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) s += v[i][e];
+    }
+  }
+  const float mean = block_sum<R_WAVES>(s, red) / D;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < R_MAXC; ++i) {
+    const int c = threadIdx.x + R_THREADS * i;
+    if (c < nch) {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const float d = v[i][e] - mean;
+        ss += d * d;
+      }
+    }
+  }
+  const float rstd = rsqrtf(block_sum<R_WAVES>(ss, red) / D + eps);
+  T* yr = y + row * D;
+#pragma unroll
+  for (int i = 0; i < R_MAXC; ++i) {
+    const int c = threadIdx.x + R_THREADS * i;
+    if (c < nch) {
+      float out[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        const int n = c * VEC + e;
+        const float xh = (v[i][e] - mean) * rstd;
+        if (mode == 0) {
+          const float sc = 1.f + p2[n] + (p3 ? p3[n] : 0.f);
+          const float sh = p0[n] + (p1 ? p1[n] : 0.f);
+          out[e] = xh * sc + sh;
+        } else {
+          out[e] = xh * p0[n] + p1[n];
+        }
+      }
+      *reinterpret_cast<u32x4*>(yr + c * VEC) = Chunk<T>::pack(out);
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0, const float* p1,
+                       const float* p2, const float* p3, float eps, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL((norm_kernel<T>), dim3(M), dim3(R_THREADS), 0, stream, x, y, D, mode, p0, p1,
+                     p2, p3, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// QK RMSNorm over the full model width (pruned channels count as zeros, so
+// the sum of squares of the kept channels is divided by D) + 3D RoPE
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int a, int nseg,
+                                                            int off0, int off1, const float* g0,
+                                                            const float* g1, float inv_dim,
+                                                            float eps, RopeDesc rope) {
+  constexpr int VEC = Chunk<T>::VEC;
+  __shared__ float red[R_WAVES];
+  const int64_t row = blockIdx.x;
+  const int nch = a / VEC;
+  // token position for RoPE
+  int pf = 0, pr = 0, pw = 0;
+  if (rope.table) {
+    const int n = (int)(row % rope.L);
+    pw = n % rope.gw;
+    pr = (n / rope.gw) % rope.gh;
+    pf = n / (rope.gw * rope.gh);
+  }
+  for (int sg = 0; sg < nseg; ++sg) {
+    T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
+    const float* gain = sg == 0 ? g0 : g1;
+    float v[R_MAXC][VEC];
+    float ss = 0.f;
+#pragma unroll
+    for (int i = 0; i < R_MAXC; ++i) {
+      const int c = threadIdx.x + R_THREADS * i;
+      if (c < nch) {
+        Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(xr + c * VEC), v[i]);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) ss += v[i][e] * v[i][e];
+      }
+    }
+    const float rstd = rsqrtf(block_sum<R_WAVES>(ss, red) * inv_dim + eps);
+#pragma unroll
+    for (int i = 0; i < R_MAXC; ++i) {
+      const int c = threadIdx.x + R_THREADS * i;
+      if (c < nch) {
+        float out[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) out[e] = v[i][e] * rstd * gain[c * VEC + e];
+        if (rope.table) {
+#pragma unroll
+          for (int e = 0; e < VEC; e += 2) {
+            const int j = ((c * VEC + e) % rope.head_dim) >> 1;
+            int idx;
+            if (j < rope.jt) {
+              idx = pf * rope.jt + j;
+            } else if (j < rope.jt + rope.jh) {
+              idx = rope.gf * rope.jt + pr * rope.jh + (j - rope.jt);
+            } else {
+              idx = rope.gf * rope.jt + rope.gh * rope.jh + pw * rope.jw + (j - rope.jt - rope.jh);
+            }
+            const float cs = rope.table[2 * idx], sn = rope.table[2 * idx + 1];
+            const float x0 = out[e], x1 = out[e + 1];
+            out[e] = x0 * cs - x1 * sn;
+            out[e + 1] = x0 * sn + x1 * cs;
+          }
+        }
+        *reinterpret_cast<u32x4*>(xr + c * VEC) = Chunk<T>::pack(out);
+      }
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off0, int off1,
+                          const float* g0, const float* g1, float inv_norm_dim, float eps,
+                          const RopeDesc* rope, hipStream_t stream) {
+  if (rows <= 0 || a <= 0) return hipSuccess;
+  RopeDesc rd{};
+  if (rope) rd = *rope;
+  hipLaunchKernelGGL((qk_norm_kernel<T>), dim3(rows), dim3(R_THREADS), 0, stream, buf, ld, a, nseg,
+                     off0, off1, g0, g1, inv_norm_dim, eps, rd);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// V -> V^T per sample, 64 x 64 tiles through LDS, zero-filled key padding
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void transpose_vt_kernel(const T* __restrict__ src,
+                                                                 int64_t lds, int a, int Lk,
+                                                                 T* __restrict__ vt, int64_t ldvt) {
+  __shared__ float tile[64][65];
+  const int j0 = blockIdx.x * 64, c0 = blockIdx.y * 64, b = blockIdx.z;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int jj = ty; jj < 64; jj += R_WAVES) {
+    const int j = j0 + jj, c = c0 + tx;
+    float v = 0.f;
+    if (j < Lk && c < a) v = to_f32(src[((int64_t)b * Lk + j) * lds + c]);
+    tile[jj][tx] = v;
+  }
+  __syncthreads();
+  for (int cc = ty; cc < 64; cc += R_WAVES) {
+    const int c = c0 + cc, j = j0 + tx;
+    if (c < a && j < ldvt) vt[((int64_t)b * a + c) * ldvt + j] = from_f32<T>(tile[tx][cc]);
+  }
+}
+
+template <typename T>
+hipError_t launch_transpose_vt(const T* src, int64_t lds, int a, int B, int Lk, T* Vt,
+                               int64_t ldvt, hipStream_t stream) {
+  if (a <= 0 || B <= 0) return hipSuccess;
+  dim3 grid((unsigned)((ldvt + 63) / 64), (unsigned)((a + 63) / 64), (unsigned)B);
+  hipLaunchKernelGGL((transpose_vt_kernel<T>), grid, dim3(R_THREADS), 0, stream, src, lds, a, Lk,
+                     Vt, ldvt);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// plan-time gather of kept rows / columns
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void gather_kernel(const T* __restrict__ src, int64_t lds,
+                                                           T* __restrict__ dst, int64_t ldd,
+                                                           int cols, const int32_t* ridx,
+                                                           const int32_t* cidx) {
+  const int64_t r = blockIdx.x;
+  const int sr = ridx ? ridx[r] : (int)r;
+  for (int c = threadIdx.x; c < cols; c += R_THREADS) {
+    const int sc = cidx ? cidx[c] : c;
+    T v = from_f32<T>(0.f);
+    if (sr >= 0 && sc >= 0) v = src[(int64_t)sr * lds + sc];
+    dst[r * ldd + c] = v;
+  }
+}
+
+template <typename T>
+hipError_t launch_gather(const T* src, int64_t lds, T* dst, int64_t ldd, int rows, int cols,
+                         const int32_t* ridx, const int32_t* cidx, hipStream_t stream) {
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gather_kernel<T>), dim3(rows), dim3(R_THREADS), 0, stream, src, lds, dst, ldd,
+                     cols, ridx, cidx);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// timestep embedding pieces
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void gemv_kernel(const T* __restrict__ W,
+                                                         const float* __restrict__ x,
+                                                         const float* __restrict__ bias,
+                                                         float* __restrict__ out, int N, int K) {
+  constexpr int VEC = Chunk<T>::VEC;
+  const int n = blockIdx.x * R_WAVES + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (n >= N) return;
+  const T* wr = W + (int64_t)n * K;
+  float acc = 0.f;
+  for (int k = lane * VEC; k < K; k += kWave * VEC) {
+    float w[VEC];
+    Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(wr + k), w);
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc += w[e] * x[k + e];
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) out[n] = acc + (bias ? bias[n] : 0.f);
+}
+
+template <typename T>
+hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out, int N, int K,
+                       hipStream_t stream) {
+  if (N <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemv_kernel<T>), dim3((N + R_WAVES - 1) / R_WAVES), dim3(R_THREADS), 0, stream,
+                     W, x, bias, out, N, K);
+  return hipGetLastError();
+}
+
+// [cos(t w_j), sin(t w_j)], w_j = 10000^(-j/half), in double precision:
+// t w_j reaches ~1e3 rad, where a float argument already loses 1e-4.
+__global__ void sinusoid_kernel(float t, int half, float* out) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= half) return;
+  const double arg = (double)t * pow(10000.0, -(double)j / (double)half);
+  out[j] = (float)cos(arg);
+  out[half + j] = (float)sin(arg);
+}
+
+hipError_t launch_sinusoid(float t, int dim, float* out, hipStream_t stream) {
+  const int half = dim / 2;
+  hipLaunchKernelGGL(sinusoid_kernel, dim3((half + 255) / 256), dim3(256), 0, stream, t, half, out);
+  return hipGetLastError();
+}
+
+__global__ void silu_kernel(const float* x, float* y, int n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) y[i] = x[i] / (1.f + expf(-x[i]));
+}
+
+hipError_t launch_silu(const float* x, float* y, int n, hipStream_t stream) {
+  hipLaunchKernelGGL(silu_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, x, y, n);
+  return hipGetLastError();
+}
+
+__global__ void euler_kernel(float* z, const float* v, float dsig, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    z[i] = fmaf(dsig, v[i], z[i]);
+}
+
+hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL(euler_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, z, v, dsig, n);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void cast_kernel(const float* src, T* dst, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x)
+    dst[i] = from_f32<T>(src[i]);
+}
+
+template <typename T>
+hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL((cast_kernel<T>), dim3((unsigned)blocks), dim3(256), 0, stream, src, dst, n);
+  return hipGetLastError();
+}
+
+#define INST(T)                                                                                \
+  template hipError_t launch_norm<T>(const T*, T*, int, int, int, const float*, const float*,  \
+                                     const float*, const float*, float, hipStream_t);          \
+  template hipError_t launch_qk_norm<T>(T*, int64_t, int, int, int, int, int, const float*,    \
+                                        const float*, float, float, const RopeDesc*,           \
+                                        hipStream_t);                                          \
+  template hipError_t launch_transpose_vt<T>(const T*, int64_t, int, int, int, T*, int64_t,    \
+                                             hipStream_t);                                     \
+  template hipError_t launch_gather<T>(const T*, int64_t, T*, int64_t, int, int,               \
+                                       const int32_t*, const int32_t*, hipStream_t);           \
+  template hipError_t launch_gemv<T>(const T*, const float*, const float*, float*, int, int,   \
+                                     hipStream_t);                                             \
+  template hipError_t launch_cast<T>(const float*, T*, int64_t, hipStream_t);
+INST(float)
+INST(bf16)
+#undef INST
+
+}  // namespace dif

@@ -1,0 +1,109 @@
+"""Operator-level parity of the hot kernels through the C ABI.
+
+GEMM: C = A B^T (its plain definition, numpy float64 matmul on the same
+inputs).  Attention: the oracle's two-pass softmax attention on the same
+inputs.  Shapes span several tiles with ragged tails in every dimension.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_06631_amd import binding as B
+from tests.gpu_util import rel_err, say, to_np
+from workloads.synth import bf16_round
+
+pytestmark = pytest.mark.gpu
+
+
+def _rand(g, shape, scale=1.0, bf16=True):
+    a = g.standard_normal(shape, dtype=np.float32) * np.float32(scale)
+    return bf16_round(a) if bf16 else a
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("M,N,K", [(1, 64, 64), (300, 200, 128), (517, 1152, 256), (1000, 640, 0),
+                                   (2100, 768, 1536)])
+def test_gemm_store_matches_matmul(dtype, M, N, K):
+    import torch
+    say(f"gemm store {dtype} M={M} N={N} K={K}")
+    g = np.random.default_rng(M + N + K)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    a, b = _rand(g, (M, K), bf16=bf), _rand(g, (N, K), bf16=bf)
+    bias = g.standard_normal(N).astype(np.float32)
+    A = torch.from_numpy(a).cuda().to(tdt)
+    Bm = torch.from_numpy(b).cuda().to(tdt)
+    Cf = torch.full((M, N), float("nan"), device="cuda", dtype=torch.float32)
+    B.dif_gemm(A, Bm, Cf, B.EPI_STORE, bias=torch.from_numpy(bias).cuda(), K=K)
+    torch.cuda.synchronize()
+    ref = a.astype(np.float64) @ b.astype(np.float64).T + bias
+    tol = 1e-5 if K else 0.0
+    assert rel_err(to_np(Cf), ref) <= tol
+    if bf:  # bf16 output: one extra rounding
+        Cb = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        B.dif_gemm(A, Bm, Cb, B.EPI_STORE, bias=torch.from_numpy(bias).cuda(), K=K)
+        torch.cuda.synchronize()
+        assert rel_err(to_np(Cb), ref) <= 8e-3
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_gemm_gelu_and_residual_epilogues(dtype):
+    import torch
+    say(f"gemm epilogues {dtype}")
+    g = np.random.default_rng(7)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    M, N, K = 777, 320, 192
+    a, b = _rand(g, (M, K), 0.5, bf), _rand(g, (N, K), 0.5, bf)
+    bias = g.standard_normal(N).astype(np.float32)
+    g0, g1 = g.standard_normal(N).astype(np.float32), g.standard_normal(N).astype(np.float32)
+    x0 = _rand(g, (M, N), 1.0, bf)
+    A, Bm = torch.from_numpy(a).cuda().to(tdt), torch.from_numpy(b).cuda().to(tdt)
+    acc = a.astype(np.float64) @ b.astype(np.float64).T + bias
+    C = torch.empty((M, N), device="cuda", dtype=tdt)
+    B.dif_gemm(A, Bm, C, B.EPI_GELU, bias=torch.from_numpy(bias).cuda())
+    X = torch.from_numpy(x0).cuda().to(tdt)
+    B.dif_gemm(A, Bm, X, B.EPI_RESIDUAL, bias=torch.from_numpy(bias).cuda(),
+               gate0=torch.from_numpy(g0).cuda(), gate1=torch.from_numpy(g1).cuda())
+    torch.cuda.synchronize()
+    tol = 8e-3 if bf else 1e-5
+    assert rel_err(to_np(C), O.gelu_tanh(acc)) <= tol
+    assert rel_err(to_np(X), x0 + (g0 + g1) * acc) <= tol
+
+
+def _attn_case(dtype, dh, H, Lq, Lk, Bn=1, qscale=1.0, seed=0):
+    import torch
+    g = np.random.default_rng(seed)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    W = H * dh
+    q = _rand(g, (Bn, Lq, W), qscale, bf)
+    k = _rand(g, (Bn, Lk, W), 1.0, bf)
+    v = _rand(g, (Bn, Lk, W), 1.0, bf)
+    ldvt = -(-Lk // 64) * 64 + 64       # padded, garbage in the pad
+    vt = np.full((Bn, W, ldvt), np.nan, np.float32)
+    vt[:, :, :Lk] = v.transpose(0, 2, 1)
+    Q, K = torch.from_numpy(q).cuda().to(tdt), torch.from_numpy(k).cuda().to(tdt)
+    Vt = torch.from_numpy(vt).cuda().to(tdt)
+    Ot = torch.full((Bn, Lq, W), float("nan"), device="cuda", dtype=tdt)
+    B.dif_attention(Q, K, Vt, Ot, Bn, Lq, Lk, H, dh, W, W, ldvt, W)
+    torch.cuda.synchronize()
+    got = to_np(Ot)
+    ref = np.stack([O.attention(q[b].astype(np.float64), k[b].astype(np.float64),
+                                v[b].astype(np.float64), H, dh) for b in range(Bn)])
+    return rel_err(got, ref)
+
+
+@pytest.mark.parametrize("dtype,dh", [("bf16", 128), ("f32", 64), ("f32", 128), ("bf16", 64)])
+@pytest.mark.parametrize("Lq,Lk", [(128, 64), (333, 517), (70, 5), (1, 1)])
+def test_attention_matches_oracle(dtype, dh, Lq, Lk):
+    say(f"attention {dtype} dh={dh} Lq={Lq} Lk={Lk}")
+    err = _attn_case(dtype, dh, 3, Lq, Lk, Bn=2, qscale=3.0, seed=Lq + Lk)
+    assert err <= (2e-2 if dtype == "bf16" else 1e-5)
+
+
+def test_attention_long_keys_online_softmax():
+    say("attention bf16 long keys")
+    # sharp scores that keep moving the running max across many key tiles
+    err = _attn_case("bf16", 128, 2, 300, 4099, Bn=1, qscale=4.0, seed=11)
+    assert err <= 2e-2
