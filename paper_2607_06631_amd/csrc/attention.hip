@@ -8,16 +8,18 @@
 // Q^T (columns = queries), held in registers for the whole key loop.  A lane
 // then owns one query column and 16 keys of each 32-key tile, so the
 // softmax row statistics are lane-local plus one exchange with lane^32.
-// The K rows are placed in LDS in the order pi(i) = 16*(i/4 % 2) + ...
-// chosen so that accumulator register r of lane group g holds key
-// 16*g + r: each lane group's 16 probabilities are consecutive keys, which
+// The K rows are placed in LDS in a permuted order (key_slot) chosen so that
+// accumulator register r of lane group g holds key 16*g + r: each lane group's 16 probabilities are consecutive keys, which
 // makes them directly the B operand (P^T) of O^T += V^T P^T, and makes the
 // matching V^T operand one contiguous 16-byte LDS read.  V is consumed
 // transposed (Vt, [head_dim rows][keys]) so that read is row-contiguous.
 //
-// Online softmax in base 2 (scores pre-multiplied by log2(e)/sqrt(dh));
-// the O^T rescale is skipped when no lane's running max moved.  Key tails
-// are masked to -inf; V^T chunks past the last key are zero-filled.
+// Online softmax in base 2 (scores pre-multiplied by log2(e)/sqrt(dh))
+// with a lazy rescale: the exponent base only moves (and O^T, l are
+// rescaled) when a query's running max exceeds it by more than kSlack.
+// Key tails are masked to -inf; V^T chunks past the last key are zero-filled.
+// At most 256 registers per lane, so two waves share each SIMD and one
+// wave's softmax overlaps the other's MFMA work.
 #include "common.h"
 #include "kernels.h"
 
@@ -26,6 +28,7 @@ namespace dif {
 constexpr int AT_THREADS = 256;
 constexpr int AT_BM = 128;  // queries per workgroup
 constexpr int AT_BN = 64;   // keys per tile
+constexpr float kSlack = 8.f;  // log2 headroom of the lazy softmax rescale
 
 template <typename T>
 struct AttnParams {
@@ -45,7 +48,7 @@ __device__ __forceinline__ int key_slot(int kappa) {
 }
 
 template <typename T, int DH>
-__global__ __launch_bounds__(AT_THREADS) void flash_attn_kernel(AttnParams<T> p) {
+__global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T> p) {
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int KCH = DH * (int)sizeof(T) / 16;     // chunks per K row
   constexpr int VCH = AT_BN * (int)sizeof(T) / 16;  // chunks per V^T row
@@ -163,27 +166,32 @@ __global__ __launch_bounds__(AT_THREADS) void flash_attn_kernel(AttnParams<T> p)
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kk][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * p.c);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.c;
+    // Lazy rescale: the exponent base m_run only moves when some query's
+    // max exceeds it by more than kSlack (probabilities stay <= 2^kSlack,
+    // far from float overflow); numerator and denominator share the base,
+    // so the normalised result is unchanged.
+    if (__any(mx > m_run + kSlack)) {
+      const float m_new = fmaxf(m_run, mx);
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      m_run = m_new;
+    }
     float rs = 0.f;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[kk][r], p.c, -m_new));
+        const float e = __builtin_amdgcn_exp2f(fmaf(s[kk][r], p.c, -m_run));
         s[kk][r] = e;
         rs += e;
       }
     rs += __shfl_xor(rs, 32);
-    l_run = l_run * alpha + rs;
-    if (__any(m_new != m_run)) {
-#pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-    }
-    m_run = m_new;
+    l_run += rs;
 
     // O^T += V^T P^T
 #pragma unroll

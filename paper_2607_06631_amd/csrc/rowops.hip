@@ -11,63 +11,81 @@
 namespace dif {
 
 constexpr int R_THREADS = 256;
-constexpr int R_WAVES = R_THREADS / kWave;
-constexpr int R_MAXC = 4;  // 16-byte chunks per thread per row
+constexpr int R_WAVES = R_THREADS / kWave;   // one row per wave
+constexpr int R_MAXC = 16;                   // 16-byte chunks per lane per row
 
 // ---------------------------------------------------------------------------
-// LayerNorm (biased variance, eps) + AdaLN modulation or affine
+// LayerNorm (biased variance, eps) + AdaLN modulation or affine.
+// One wave per row: the row stays in the wave's registers between the two
+// statistics passes and the apply pass; reductions are wave-local.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(R_THREADS) void norm_kernel(const T* __restrict__ x, T* __restrict__ y,
-                                                         int D, int mode, const float* p0,
+                                                         int M, int D, int mode, const float* p0,
                                                          const float* p1, const float* p2,
                                                          const float* p3, float eps) {
   constexpr int VEC = Chunk<T>::VEC;
-  __shared__ float red[R_WAVES];
-  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * R_WAVES + (threadIdx.x >> 6);
+  if (row >= M) return;
   const int nch = D / VEC;
   const T* xr = x + row * D;
-  float v[R_MAXC][VEC];
+  u32x4 raw[R_MAXC];  // the row slice stays packed in registers
   float s = 0.f;
 #pragma unroll
   for (int i = 0; i < R_MAXC; ++i) {
-    const int c = threadIdx.x + R_THREADS * i;
+    const int c = lane + kWave * i;
     if (c < nch) {
-      Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(xr + c * VEC), v[i]);
+      raw[i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+      float v[VEC];
+      Chunk<T>::unpack(raw[i], v);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) s += v[i][e];
+      for (int e = 0; e < VEC; ++e) s += v[e];
     }
   }
-  const float mean = block_sum<R_WAVES>(s, red) / D;
+  const float mean = wave_sum(s) / D;
   float ss = 0.f;
 #pragma unroll
   for (int i = 0; i < R_MAXC; ++i) {
-    const int c = threadIdx.x + R_THREADS * i;
+    const int c = lane + kWave * i;
     if (c < nch) {
+      float v[VEC];
+      Chunk<T>::unpack(raw[i], v);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
-        const float d = v[i][e] - mean;
+        const float d = v[e] - mean;
         ss += d * d;
       }
     }
   }
-  const float rstd = rsqrtf(block_sum<R_WAVES>(ss, red) / D + eps);
+  const float rstd = rsqrtf(wave_sum(ss) / D + eps);
   T* yr = y + row * D;
 #pragma unroll
   for (int i = 0; i < R_MAXC; ++i) {
-    const int c = threadIdx.x + R_THREADS * i;
+    const int c = lane + kWave * i;
     if (c < nch) {
-      float out[VEC];
+      float v[VEC], out[VEC];
+      Chunk<T>::unpack(raw[i], v);
+      const int n0 = c * VEC;
+      if (mode == 0) {
+        const f32x4* a0 = reinterpret_cast<const f32x4*>(p0 + n0);
+        const f32x4* a2 = reinterpret_cast<const f32x4*>(p2 + n0);
 #pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const int n = c * VEC + e;
-        const float xh = (v[i][e] - mean) * rstd;
-        if (mode == 0) {
-          const float sc = 1.f + p2[n] + (p3 ? p3[n] : 0.f);
-          const float sh = p0[n] + (p1 ? p1[n] : 0.f);
-          out[e] = xh * sc + sh;
-        } else {
-          out[e] = xh * p0[n] + p1[n];
+        for (int q = 0; q < VEC / 4; ++q) {
+          f32x4 sh = a0[q], sc = a2[q];
+          if (p1) sh += reinterpret_cast<const f32x4*>(p1 + n0)[q];
+          if (p3) sc += reinterpret_cast<const f32x4*>(p3 + n0)[q];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            out[4 * q + e] = (v[4 * q + e] - mean) * rstd * (1.f + sc[e]) + sh[e];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < VEC / 4; ++q) {
+          const f32x4 w = reinterpret_cast<const f32x4*>(p0 + n0)[q];
+          const f32x4 b = reinterpret_cast<const f32x4*>(p1 + n0)[q];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) out[4 * q + e] = (v[4 * q + e] - mean) * rstd * w[e] + b[e];
         }
       }
       *reinterpret_cast<u32x4*>(yr + c * VEC) = Chunk<T>::pack(out);
@@ -79,25 +97,26 @@ template <typename T>
 hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0, const float* p1,
                        const float* p2, const float* p3, float eps, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL((norm_kernel<T>), dim3(M), dim3(R_THREADS), 0, stream, x, y, D, mode, p0, p1,
-                     p2, p3, eps);
+  hipLaunchKernelGGL((norm_kernel<T>), dim3((M + R_WAVES - 1) / R_WAVES), dim3(R_THREADS), 0, stream,
+                     x, y, M, D, mode, p0, p1, p2, p3, eps);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
 // QK RMSNorm over the full model width (pruned channels count as zeros, so
-// the sum of squares of the kept channels is divided by D) + 3D RoPE
+// the sum of squares of the kept channels is divided by D) + 3D RoPE.
+// One wave per row.
 // ---------------------------------------------------------------------------
 template <typename T>
-__global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int a, int nseg,
-                                                            int off0, int off1, const float* g0,
-                                                            const float* g1, float inv_dim,
-                                                            float eps, RopeDesc rope) {
+__global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
+                                                            int nseg, int off0, int off1,
+                                                            const float* g0, const float* g1,
+                                                            float inv_dim, float eps, RopeDesc rope) {
   constexpr int VEC = Chunk<T>::VEC;
-  __shared__ float red[R_WAVES];
-  const int64_t row = blockIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * R_WAVES + (threadIdx.x >> 6);
+  if (row >= rows) return;
   const int nch = a / VEC;
-  // token position for RoPE
   int pf = 0, pr = 0, pw = 0;
   if (rope.table) {
     const int n = (int)(row % rope.L);
@@ -108,25 +127,28 @@ __global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, 
   for (int sg = 0; sg < nseg; ++sg) {
     T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
     const float* gain = sg == 0 ? g0 : g1;
-    float v[R_MAXC][VEC];
+    u32x4 raw[R_MAXC];
     float ss = 0.f;
 #pragma unroll
     for (int i = 0; i < R_MAXC; ++i) {
-      const int c = threadIdx.x + R_THREADS * i;
+      const int c = lane + kWave * i;
       if (c < nch) {
-        Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(xr + c * VEC), v[i]);
+        raw[i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+        float v[VEC];
+        Chunk<T>::unpack(raw[i], v);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) ss += v[i][e] * v[i][e];
+        for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
       }
     }
-    const float rstd = rsqrtf(block_sum<R_WAVES>(ss, red) * inv_dim + eps);
+    const float rstd = rsqrtf(wave_sum(ss) * inv_dim + eps);
 #pragma unroll
     for (int i = 0; i < R_MAXC; ++i) {
-      const int c = threadIdx.x + R_THREADS * i;
+      const int c = lane + kWave * i;
       if (c < nch) {
         float out[VEC];
+        Chunk<T>::unpack(raw[i], out);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) out[e] = v[i][e] * rstd * gain[c * VEC + e];
+        for (int e = 0; e < VEC; ++e) out[e] *= rstd * gain[c * VEC + e];
         if (rope.table) {
 #pragma unroll
           for (int e = 0; e < VEC; e += 2) {
@@ -147,6 +169,8 @@ __global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, 
         }
         *reinterpret_cast<u32x4*>(xr + c * VEC) = Chunk<T>::pack(out);
       }
+      // keep the per-chunk gain / table loads from being hoisted en masse
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 }
@@ -158,8 +182,8 @@ hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off
   if (rows <= 0 || a <= 0) return hipSuccess;
   RopeDesc rd{};
   if (rope) rd = *rope;
-  hipLaunchKernelGGL((qk_norm_kernel<T>), dim3(rows), dim3(R_THREADS), 0, stream, buf, ld, a, nseg,
-                     off0, off1, g0, g1, inv_norm_dim, eps, rd);
+  hipLaunchKernelGGL((qk_norm_kernel<T>), dim3((rows + R_WAVES - 1) / R_WAVES), dim3(R_THREADS), 0,
+                     stream, buf, ld, rows, a, nseg, off0, off1, g0, g1, inv_norm_dim, eps, rd);
   return hipGetLastError();
 }
 
