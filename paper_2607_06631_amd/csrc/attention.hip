@@ -115,13 +115,13 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
       const int id = tid + AT_THREADS * i;
       const int kl = id / KCH, c = id % KCH;
       const int row = (kl & ~31) + key_slot(kl & 31);
-      ks_[buf][row][c ^ (row & 7)] = kreg[i];
+      ks_[buf][row][swz<KCH>(row, c)] = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
       const int id = tid + AT_THREADS * i;
       const int d = id / VCH, c = id % VCH;
-      vs_[buf][d][c ^ (d & 7)] = vreg[i];
+      vs_[buf][d][swz<VCH>(d, c)] = vreg[i];
     }
   };
 
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
       for (int r = 0; r < 16; ++r) s[kk][r] = 0.f;
 #pragma unroll
       for (int st = 0; st < NQS; ++st) {
-        const u32x4 a = ks_[buf][kk * 32 + col][(2 * st + g) ^ (col & 7)];
+        const u32x4 a = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * st + g)];
         Mma<T>::step(s[kk], a, qf[st]);
       }
     }
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
         const int vc = (kk * 32 + 16 * g) / VEC + u;
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) {
-          const u32x4 a = vs_[buf][dt * 32 + col][vc ^ (col & 7)];
+          const u32x4 a = vs_[buf][dt * 32 + col][swz<VCH>(col, vc)];
           Mma<T>::step(o[dt], a, pc);
         }
       }

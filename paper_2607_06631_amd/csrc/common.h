@@ -89,24 +89,25 @@ __device__ __forceinline__ int xcd_remap(int bid, int total) {
   return (x < r) ? x * (q + 1) + local : r * (q + 1) + (x - r) * q + local;
 }
 
+// LDS position of 16-byte chunk c in row `row` of a tile whose rows hold CH
+// chunks.  A wave's 16-byte LDS accesses are served in groups of lanes
+// that read consecutive rows at the same logical chunk; the XOR makes
+// every group of 8 lanes (128-byte window) and of 16 lanes (256-byte
+// window) hit distinct banks, for row-contiguous writes as well.
+template <int CH>
+__device__ __forceinline__ int swz(int row, int c) {
+  static_assert(CH == 8 || CH >= 16, "LDS rows of 8 or >= 16 chunks");
+  if constexpr (CH == 8) {
+    return c ^ ((row & 7) ^ ((row >> 3) & 1));
+  } else {
+    return c ^ (row & 15);
+  }
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
   return v;
-}
-
-// Sum over a workgroup of `nwaves` waves; every thread gets the total.
-template <int NWAVES>
-__device__ __forceinline__ float block_sum(float v, float* red /* [NWAVES] */) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) red[w] = v;
-  __syncthreads();
-  float t = 0.f;
-#pragma unroll
-  for (int i = 0; i < NWAVES; ++i) t += red[i];
-  return t;
 }
 
 __device__ __forceinline__ float gelu_tanh(float x) {
@@ -114,7 +115,5 @@ __device__ __forceinline__ float gelu_tanh(float x) {
   const float u = c * (x + 0.044715f * x * x * x);
   return 0.5f * x * (1.f + tanhf(u));
 }
-
-__device__ __forceinline__ float silu(float x) { return x / (1.f + __expf(-x)); }
 
 }  // namespace dif

@@ -3,20 +3,20 @@
 // Both operands are K-contiguous (nn.Linear layout), which is exactly the
 // per-lane layout the MFMA operands want: every lane feeds a 16-byte run of
 // consecutive k.  Workgroup tile 256 x 256, k-tile 128 bytes per row (64
-// bf16 / 32 f32), 8 waves arranged 2 (M) x 4 (N), each owning a 128 x 64
-// block = 4 x 2 MFMA 32x32 tiles.  Operand tiles are staged through LDS,
-// double-buffered (2 x 64 KB of the 160 KB LDS), with the 16-byte chunks of
-// each row XOR-swizzled by (row & 7) so both the row-contiguous stores and
-// the 32-row fragment reads are bank-conflict free.  Ragged M and N are
-// handled by clamping the load rows and predicating the stores; K must be a
-// multiple of the k-tile (the plan pads pruned widths to 64).
+// bf16 / 32 f32), split over a grid of waves that each own a block of
+// MFMA 32x32 tiles.  Operand tiles are staged through LDS, double-buffered
+// (2 x 64 KB of the 160 KB LDS), with the 16-byte chunks of each row
+// XOR-swizzled (swz) so both the row-contiguous stores and the 32-row
+// fragment reads are bank-conflict free.  Global loads (buffer loads on
+// block-local descriptors) run two k-tiles ahead through two register
+// staging sets.  Ragged M and N: rows past the matrix read as zero through
+// the descriptor bounds and stores are predicated; K must be a multiple of
+// the k-tile (the plan pads pruned widths to 64).
 #include "common.h"
 #include "kernels.h"
 
 namespace dif {
 
-constexpr int G_BM = 256, G_BN = 256;
-constexpr int G_THREADS = 512;
 constexpr int G_CH = 8;  // 16-byte chunks per k-tile row (128 bytes)
 
 template <typename T, typename OutT>
@@ -31,113 +31,137 @@ struct GemmParams {
   const float* gate1;
 };
 
-template <typename T, typename OutT, int EPI>
-__global__ __launch_bounds__(G_THREADS) void gemm_nt_kernel(GemmParams<T, OutT> p) {
-  __shared__ u32x4 smem[2][G_BM + G_BN][G_CH];
+// WGM x WGN waves; each wave owns TM x TN MFMA 32x32 tiles.
+template <typename T, typename OutT, int EPI, int WGM, int WGN, int TM, int TN>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, OutT> p) {
+  constexpr int NT = 64 * WGM * WGN;
+  constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int BK = G_CH * VEC;
+  constexpr int RPL = NT / G_CH;          // rows covered by one staging pass
+  constexpr int LA = BM / RPL, LB = BN / RPL;
+  static_assert(LA * RPL == BM && LB * RPL == BN, "staging split");
+  __shared__ u32x4 smem[2][BM + BN][G_CH];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int g = lane >> 5, col = lane & 31;
 
   // logical tile: XCD-contiguous ranges, then groups of GM row-tiles that
   // walk the N tiles together (operand reuse in L2)
-  const int nbm = (p.M + G_BM - 1) / G_BM, nbn = (p.N + G_BN - 1) / G_BN;
+  const int nbm = (p.M + BM - 1) / BM, nbn = (p.N + BN - 1) / BN;
   const int bid = xcd_remap(blockIdx.x, nbm * nbn);
   constexpr int GM = 8;
   const int group = bid / (GM * nbn);
   const int first_m = group * GM;
   const int gsize = min(nbm - first_m, GM);
   const int in_group = bid - group * GM * nbn;
-  const int m0 = (first_m + in_group % gsize) * G_BM;
-  const int n0 = (in_group / gsize) * G_BN;
+  const int m0 = (first_m + in_group % gsize) * BM;
+  const int n0 = (in_group / gsize) * BN;
 
-  // global -> LDS staging: thread loads chunk lc of rows lr + 64 i
+  // global -> LDS staging: thread loads chunk lc of rows lr + RPL * i with
+  // buffer loads against block-local descriptors; rows past M / N fall
+  // outside the descriptor and read as zero.
   const int lc = tid & 7, lr = tid >> 3;
-  const T* a_src[4];
-  const T* b_src[4];
+  constexpr uint32_t kRsrcWord3 = 0x00020000u;
+  const uint32_t a_bytes = (uint32_t)(min(BM, p.M - m0) * p.lda * (int64_t)sizeof(T));
+  const uint32_t b_bytes = (uint32_t)(min(BN, p.N - n0) * p.ldb * (int64_t)sizeof(T));
+  const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>(p.A + (int64_t)m0 * p.lda), (short)0, a_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>(p.B + (int64_t)n0 * p.ldb), (short)0, b_bytes, kRsrcWord3);
+  uint32_t a_off[LA], b_off[LB];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int ra = min(m0 + lr + 64 * i, p.M - 1);
-    const int rb = min(n0 + lr + 64 * i, p.N - 1);
-    a_src[i] = p.A + (int64_t)ra * p.lda + lc * VEC;
-    b_src[i] = p.B + (int64_t)rb * p.ldb + lc * VEC;
-  }
-  u32x4 ra_reg[4], rb_reg[4];
+  for (int i = 0; i < LA; ++i)
+    a_off[i] = (uint32_t)(((lr + RPL * i) * p.lda + lc * VEC) * (int64_t)sizeof(T));
+#pragma unroll
+  for (int i = 0; i < LB; ++i)
+    b_off[i] = (uint32_t)(((lr + RPL * i) * p.ldb + lc * VEC) * (int64_t)sizeof(T));
   const int nk = p.K / BK;
 
-  f32x16 acc[4][2];
+  // Two register staging sets: tile kt+2 is requested while tile kt is
+  // computed, so global latency is hidden behind two compute phases.
+  u32x4 ra0[LA], rb0[LB], ra1[LA], rb1[LB];
+  auto gload = [&](int kt, u32x4* ra, u32x4* rb) {
+    const int koff = kt * BK * (int)sizeof(T);
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < LA; ++i)
+      ra[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_off[i], koff, 0));
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int i = 0; i < LB; ++i)
+      rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i], koff, 0));
+  };
+  auto sstore = [&](int buf, const u32x4* ra, const u32x4* rb) {
+#pragma unroll
+    for (int i = 0; i < LA; ++i) {
+      const int row = lr + RPL * i;
+      smem[buf][row][swz<G_CH>(row, lc)] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < LB; ++i) {
+      const int row = lr + RPL * i;
+      smem[buf][BM + row][swz<G_CH>(row, lc)] = rb[i];
+    }
+  };
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  if (nk > 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      ra_reg[i] = *reinterpret_cast<const u32x4*>(a_src[i]);
-      rb_reg[i] = *reinterpret_cast<const u32x4*>(b_src[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = lr + 64 * i;
-      smem[0][row][lc ^ (row & 7)] = ra_reg[i];
-      smem[0][G_BM + row][lc ^ (row & 7)] = rb_reg[i];
-    }
-  }
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int64_t off = (int64_t)(kt + 1) * BK;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        ra_reg[i] = *reinterpret_cast<const u32x4*>(a_src[i] + off);
-        rb_reg[i] = *reinterpret_cast<const u32x4*>(b_src[i] + off);
-      }
-    }
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int ks = 0; ks < G_CH / 2; ++ks) {
-      const int c = (2 * ks + g) ^ (col & 7);
-      u32x4 af[4], bfr[2];
+      const int c = swz<G_CH>(col, 2 * ks + g);   // rows are col + multiples of 32
+      u32x4 af[TM], bfr[TN];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) af[i] = smem[buf][wm * 128 + i * 32 + col][c];
+      for (int i = 0; i < TM; ++i) af[i] = smem[buf][wm * TM * 32 + i * 32 + col][c];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) bfr[j] = smem[buf][G_BM + wn * 64 + j * 32 + col][c];
+      for (int j = 0; j < TN; ++j) bfr[j] = smem[buf][BM + wn * TN * 32 + j * 32 + col][c];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) Mma<T>::step(acc[i][j], af[i], bfr[j]);
+        for (int j = 0; j < TN; ++j) Mma<T>::step(acc[i][j], af[i], bfr[j]);
     }
-    if (more) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = lr + 64 * i;
-        smem[buf ^ 1][row][lc ^ (row & 7)] = ra_reg[i];
-        smem[buf ^ 1][G_BM + row][lc ^ (row & 7)] = rb_reg[i];
-      }
-    }
+  };
+  // one k-tile: `cur` holds the tile after kt (stored at the end), `nxt`
+  // receives tile kt + 2
+  auto ktile = [&](int kt, u32x4* ra_cur, u32x4* rb_cur, u32x4* ra_nxt, u32x4* rb_nxt) {
+    if (kt + 2 < nk) gload(kt + 2, ra_nxt, rb_nxt);
+    compute(kt & 1);
+    if (kt + 1 < nk) sstore((kt + 1) & 1, ra_cur, rb_cur);
     __syncthreads();
+  };
+
+  if (nk > 0) {
+    gload(0, ra0, rb0);
+    sstore(0, ra0, rb0);
+    if (nk > 1) gload(1, ra1, rb1);
   }
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    ktile(kt, ra1, rb1, ra0, rb0);       // tile kt+1 is in set 1, kt+2 goes to set 0
+    ktile(kt + 1, ra0, rb0, ra1, rb1);   // tile kt+2 is in set 0, kt+3 goes to set 1
+  }
+  if (kt < nk) ktile(kt, ra1, rb1, ra0, rb0);
 
   // epilogue: lane holds column n of each tile, 16 rows
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int n = n0 + wn * 64 + j * 32 + col;
+  for (int j = 0; j < TN; ++j) {
+    const int n = n0 + wn * TN * 32 + j * 32 + col;
     if (n >= p.N) continue;
     const float bias = p.bias ? p.bias[n] : 0.f;
     float gate = 1.f;
     if (EPI == EPI_RESIDUAL && p.gate0) gate = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * 128 + i * 32 + acc_row(r, g);
+        const int m = m0 + wm * TM * 32 + i * 32 + acc_row(r, g);
         if (m < p.M) {
           OutT* dst = p.C + (int64_t)m * p.ldc + n;
           const float v = acc[i][j][r] + bias;
@@ -154,18 +178,35 @@ __global__ __launch_bounds__(G_THREADS) void gemm_nt_kernel(GemmParams<T, OutT> 
   }
 }
 
+// Tile shapes: 256 x 256 workgroup tile as 8 waves of 128 x 64 (default)
+// or 4 waves of 128 x 128.
+#ifndef DIF_GEMM_WAVES
+#define DIF_GEMM_WAVES 8
+#endif
+
+template <typename T, typename OutT, int EPI>
+void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
+#if DIF_GEMM_WAVES == 4
+  constexpr int WGM = 2, WGN = 2, TM = 4, TN = 4;
+#else
+  constexpr int WGM = 2, WGN = 4, TM = 4, TN = 2;
+#endif
+  constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
+  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI, WGM, WGN, TM, TN>), dim3(tiles),
+                     dim3(64 * WGM * WGN), 0, stream, p);
+}
+
 template <typename T, typename OutT>
 hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
                        const float* gate1, hipStream_t stream) {
   if (M <= 0 || N <= 0) return hipSuccess;
   GemmParams<T, OutT> p{A, B, C, lda, ldb, ldc, M, N, K, bias, gate0, gate1};
-  const int tiles = ((M + G_BM - 1) / G_BM) * ((N + G_BN - 1) / G_BN);
-  dim3 grid(tiles), block(G_THREADS);
   switch (epi) {
-    case EPI_STORE: hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI_STORE>), grid, block, 0, stream, p); break;
-    case EPI_GELU: hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI_GELU>), grid, block, 0, stream, p); break;
-    default: hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI_RESIDUAL>), grid, block, 0, stream, p); break;
+    case EPI_STORE: launch_tile<T, OutT, EPI_STORE>(p, stream); break;
+    case EPI_GELU: launch_tile<T, OutT, EPI_GELU>(p, stream); break;
+    default: launch_tile<T, OutT, EPI_RESIDUAL>(p, stream); break;
   }
   return hipGetLastError();
 }

@@ -11,13 +11,18 @@
 namespace dif {
 
 constexpr int R_THREADS = 256;
-constexpr int R_WAVES = R_THREADS / kWave;   // one row per wave
-constexpr int R_MAXC = 16;                   // 16-byte chunks per lane per row
+constexpr int R_WAVES = R_THREADS / kWave;
+constexpr int R_MAXC = 16;   // 16-byte chunks per lane per row (D <= 1024 * VEC)
+constexpr int R_RPW = 8;     // rows per wave
+constexpr int R_ROWS = R_WAVES * R_RPW;
 
 // ---------------------------------------------------------------------------
 // LayerNorm (biased variance, eps) + AdaLN modulation or affine.
-// One wave per row: the row stays in the wave's registers between the two
-// statistics passes and the apply pass; reductions are wave-local.
+// The workgroup first folds the per-column vectors into LDS (shift and
+// 1 + scale, or weight and bias); each wave then normalises R_RPW rows, one
+// row at a time: one statistics pass (sum and sum of squares of the row
+// shifted by its first element) with the row kept packed in registers, then
+// the apply pass.  Reductions are wave-local.
 // ---------------------------------------------------------------------------
 template <typename T>
 __global__ __launch_bounds__(R_THREADS) void norm_kernel(const T* __restrict__ x, T* __restrict__ y,
@@ -25,110 +30,31 @@ __global__ __launch_bounds__(R_THREADS) void norm_kernel(const T* __restrict__ x
                                                          const float* p1, const float* p2,
                                                          const float* p3, float eps) {
   constexpr int VEC = Chunk<T>::VEC;
+  extern __shared__ float vec_lds[];  // [2][D]: multiplier, addend
+  float* mul = vec_lds;
+  float* add = vec_lds + D;
+  for (int n = threadIdx.x; n < D; n += R_THREADS) {
+    if (mode == 0) {
+      mul[n] = 1.f + p2[n] + (p3 ? p3[n] : 0.f);
+      add[n] = p0[n] + (p1 ? p1[n] : 0.f);
+    } else {
+      mul[n] = p0[n];
+      add[n] = p1[n];
+    }
+  }
+  __syncthreads();
   const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * R_WAVES + (threadIdx.x >> 6);
-  if (row >= M) return;
   const int nch = D / VEC;
-  const T* xr = x + row * D;
-  u32x4 raw[R_MAXC];  // the row slice stays packed in registers
-  float s = 0.f;
-#pragma unroll
-  for (int i = 0; i < R_MAXC; ++i) {
-    const int c = lane + kWave * i;
-    if (c < nch) {
-      raw[i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
-      float v[VEC];
-      Chunk<T>::unpack(raw[i], v);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) s += v[e];
-    }
-  }
-  const float mean = wave_sum(s) / D;
-  float ss = 0.f;
-#pragma unroll
-  for (int i = 0; i < R_MAXC; ++i) {
-    const int c = lane + kWave * i;
-    if (c < nch) {
-      float v[VEC];
-      Chunk<T>::unpack(raw[i], v);
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) {
-        const float d = v[e] - mean;
-        ss += d * d;
-      }
-    }
-  }
-  const float rstd = rsqrtf(wave_sum(ss) / D + eps);
-  T* yr = y + row * D;
-#pragma unroll
-  for (int i = 0; i < R_MAXC; ++i) {
-    const int c = lane + kWave * i;
-    if (c < nch) {
-      float v[VEC], out[VEC];
-      Chunk<T>::unpack(raw[i], v);
-      const int n0 = c * VEC;
-      if (mode == 0) {
-        const f32x4* a0 = reinterpret_cast<const f32x4*>(p0 + n0);
-        const f32x4* a2 = reinterpret_cast<const f32x4*>(p2 + n0);
-#pragma unroll
-        for (int q = 0; q < VEC / 4; ++q) {
-          f32x4 sh = a0[q], sc = a2[q];
-          if (p1) sh += reinterpret_cast<const f32x4*>(p1 + n0)[q];
-          if (p3) sc += reinterpret_cast<const f32x4*>(p3 + n0)[q];
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            out[4 * q + e] = (v[4 * q + e] - mean) * rstd * (1.f + sc[e]) + sh[e];
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < VEC / 4; ++q) {
-          const f32x4 w = reinterpret_cast<const f32x4*>(p0 + n0)[q];
-          const f32x4 b = reinterpret_cast<const f32x4*>(p1 + n0)[q];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) out[4 * q + e] = (v[4 * q + e] - mean) * rstd * w[e] + b[e];
-        }
-      }
-      *reinterpret_cast<u32x4*>(yr + c * VEC) = Chunk<T>::pack(out);
-    }
-  }
-}
-
-template <typename T>
-hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0, const float* p1,
-                       const float* p2, const float* p3, float eps, hipStream_t stream) {
-  if (M <= 0) return hipSuccess;
-  hipLaunchKernelGGL((norm_kernel<T>), dim3((M + R_WAVES - 1) / R_WAVES), dim3(R_THREADS), 0, stream,
-                     x, y, M, D, mode, p0, p1, p2, p3, eps);
-  return hipGetLastError();
-}
-
-// ---------------------------------------------------------------------------
-// QK RMSNorm over the full model width (pruned channels count as zeros, so
-// the sum of squares of the kept channels is divided by D) + 3D RoPE.
-// One wave per row.
-// ---------------------------------------------------------------------------
-template <typename T>
-__global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
-                                                            int nseg, int off0, int off1,
-                                                            const float* g0, const float* g1,
-                                                            float inv_dim, float eps, RopeDesc rope) {
-  constexpr int VEC = Chunk<T>::VEC;
-  const int lane = threadIdx.x & 63;
-  const int64_t row = (int64_t)blockIdx.x * R_WAVES + (threadIdx.x >> 6);
-  if (row >= rows) return;
-  const int nch = a / VEC;
-  int pf = 0, pr = 0, pw = 0;
-  if (rope.table) {
-    const int n = (int)(row % rope.L);
-    pw = n % rope.gw;
-    pr = (n / rope.gw) % rope.gh;
-    pf = n / (rope.gw * rope.gh);
-  }
-  for (int sg = 0; sg < nseg; ++sg) {
-    T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
-    const float* gain = sg == 0 ? g0 : g1;
+  const float inv_d = 1.f / (float)D;
+  for (int rr = 0; rr < R_RPW; ++rr) {
+    const int64_t row = (int64_t)blockIdx.x * R_ROWS + (threadIdx.x >> 6) * R_RPW + rr;
+    if (row >= M) break;
+    const T* xr = x + row * D;
     u32x4 raw[R_MAXC];
-    float ss = 0.f;
+    // one pass over shifted data: sum and sum of squares of (x - x0), where
+    // x0 is the row's first element, keep the variance free of cancellation
+    const float x0 = to_f32(xr[0]);
+    float s = 0.f, ss = 0.f;
 #pragma unroll
     for (int i = 0; i < R_MAXC; ++i) {
       const int c = lane + kWave * i;
@@ -137,40 +63,134 @@ __global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, 
         float v[VEC];
         Chunk<T>::unpack(raw[i], v);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
+        for (int e = 0; e < VEC; ++e) {
+          const float d = v[e] - x0;
+          s += d;
+          ss += d * d;
+        }
       }
     }
-    const float rstd = rsqrtf(wave_sum(ss) * inv_dim + eps);
+    const float ms = wave_sum(s) * inv_d;
+    const float mean = x0 + ms;
+    const float var = fmaxf(wave_sum(ss) * inv_d - ms * ms, 0.f);
+    const float rstd = rsqrtf(var + eps);
+    T* yr = y + row * D;
 #pragma unroll
     for (int i = 0; i < R_MAXC; ++i) {
       const int c = lane + kWave * i;
       if (c < nch) {
-        float out[VEC];
-        Chunk<T>::unpack(raw[i], out);
+        float v[VEC], out[VEC];
+        Chunk<T>::unpack(raw[i], v);
+        const f32x4* m4 = reinterpret_cast<const f32x4*>(mul + c * VEC);
+        const f32x4* a4 = reinterpret_cast<const f32x4*>(add + c * VEC);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) out[e] *= rstd * gain[c * VEC + e];
-        if (rope.table) {
+        for (int q = 0; q < VEC / 4; ++q) {
+          const f32x4 mu = m4[q], ad = a4[q];
 #pragma unroll
-          for (int e = 0; e < VEC; e += 2) {
-            const int j = ((c * VEC + e) % rope.head_dim) >> 1;
-            int idx;
-            if (j < rope.jt) {
-              idx = pf * rope.jt + j;
-            } else if (j < rope.jt + rope.jh) {
-              idx = rope.gf * rope.jt + pr * rope.jh + (j - rope.jt);
-            } else {
-              idx = rope.gf * rope.jt + rope.gh * rope.jh + pw * rope.jw + (j - rope.jt - rope.jh);
-            }
-            const float cs = rope.table[2 * idx], sn = rope.table[2 * idx + 1];
-            const float x0 = out[e], x1 = out[e + 1];
-            out[e] = x0 * cs - x1 * sn;
-            out[e + 1] = x0 * sn + x1 * cs;
-          }
+          for (int e = 0; e < 4; ++e) out[4 * q + e] = (v[4 * q + e] - mean) * rstd * mu[e] + ad[e];
         }
-        *reinterpret_cast<u32x4*>(xr + c * VEC) = Chunk<T>::pack(out);
+        *reinterpret_cast<u32x4*>(yr + c * VEC) = Chunk<T>::pack(out);
       }
-      // keep the per-chunk gain / table loads from being hoisted en masse
-      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_sched_barrier(0);  // bound the LDS reads kept in flight
+    }
+  }
+}
+
+template <typename T>
+hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0, const float* p1,
+                       const float* p2, const float* p3, float eps, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  hipLaunchKernelGGL((norm_kernel<T>), dim3((M + R_ROWS - 1) / R_ROWS), dim3(R_THREADS),
+                     2 * D * sizeof(float), stream, x, y, M, D, mode, p0, p1, p2, p3, eps);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// QK RMSNorm over the full model width (pruned channels count as zeros, so
+// the sum of squares of the kept channels is divided by D) + 3D RoPE.
+// Gains are staged in LDS once per workgroup.  Lane l always covers the
+// same head-local pairs (64 * VEC is a multiple of head_dim), so its
+// rotation factors are fetched once per row.
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
+                                                            int nseg, int off0, int off1,
+                                                            const float* g0, const float* g1,
+                                                            float inv_dim, float eps, RopeDesc rope) {
+  constexpr int VEC = Chunk<T>::VEC;
+  constexpr int NP = VEC / 2;  // pairs per chunk
+  extern __shared__ float gain_lds[];  // [nseg][a]
+  for (int n = threadIdx.x; n < a; n += R_THREADS) {
+    gain_lds[n] = g0[n];
+    if (nseg > 1) gain_lds[a + n] = g1[n];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63;
+  const int nch = a / VEC;
+  const int jb = ((lane * VEC) % rope.head_dim) / 2;  // first head-local pair of this lane
+  for (int rr = 0; rr < R_RPW; ++rr) {
+    const int64_t row = (int64_t)blockIdx.x * R_ROWS + (threadIdx.x >> 6) * R_RPW + rr;
+    if (row >= rows) break;
+    float cs[NP], sn[NP];
+    if (rope.table) {
+      const int n = (int)(row % rope.L);
+      const int pw = n % rope.gw, pr = (n / rope.gw) % rope.gh, pf = n / (rope.gw * rope.gh);
+#pragma unroll
+      for (int k = 0; k < NP; ++k) {
+        const int j = jb + k;
+        int idx;
+        if (j < rope.jt) {
+          idx = pf * rope.jt + j;
+        } else if (j < rope.jt + rope.jh) {
+          idx = rope.gf * rope.jt + pr * rope.jh + (j - rope.jt);
+        } else {
+          idx = rope.gf * rope.jt + rope.gh * rope.jh + pw * rope.jw + (j - rope.jt - rope.jh);
+        }
+        cs[k] = rope.table[2 * idx];
+        sn[k] = rope.table[2 * idx + 1];
+      }
+    }
+    for (int sg = 0; sg < nseg; ++sg) {
+      T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
+      const float* gain = gain_lds + sg * a;
+      u32x4 raw[R_MAXC];
+      float ss = 0.f;
+#pragma unroll
+      for (int i = 0; i < R_MAXC; ++i) {
+        const int c = lane + kWave * i;
+        if (c < nch) {
+          raw[i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+          float v[VEC];
+          Chunk<T>::unpack(raw[i], v);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
+        }
+      }
+      const float rstd = rsqrtf(wave_sum(ss) * inv_dim + eps);
+#pragma unroll
+      for (int i = 0; i < R_MAXC; ++i) {
+        const int c = lane + kWave * i;
+        if (c < nch) {
+          float out[VEC];
+          Chunk<T>::unpack(raw[i], out);
+          const f32x4* g4 = reinterpret_cast<const f32x4*>(gain + c * VEC);
+#pragma unroll
+          for (int q = 0; q < VEC / 4; ++q) {
+            const f32x4 gg = g4[q];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[4 * q + e] *= rstd * gg[e];
+          }
+          if (rope.table) {
+#pragma unroll
+            for (int k = 0; k < NP; ++k) {
+              const float x0 = out[2 * k], x1 = out[2 * k + 1];
+              out[2 * k] = x0 * cs[k] - x1 * sn[k];
+              out[2 * k + 1] = x0 * sn[k] + x1 * cs[k];
+            }
+          }
+          *reinterpret_cast<u32x4*>(xr + c * VEC) = Chunk<T>::pack(out);
+        }
+      }
     }
   }
 }
@@ -182,8 +202,12 @@ hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off
   if (rows <= 0 || a <= 0) return hipSuccess;
   RopeDesc rd{};
   if (rope) rd = *rope;
-  hipLaunchKernelGGL((qk_norm_kernel<T>), dim3((rows + R_WAVES - 1) / R_WAVES), dim3(R_THREADS), 0,
-                     stream, buf, ld, rows, a, nseg, off0, off1, g0, g1, inv_norm_dim, eps, rd);
+  if (rd.head_dim <= 0) rd.head_dim = 64;   // no rotation: any width dividing 64 * VEC
+  constexpr int VEC = Chunk<T>::VEC;
+  if ((64 * VEC) % rd.head_dim != 0) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((qk_norm_kernel<T>), dim3((rows + R_ROWS - 1) / R_ROWS), dim3(R_THREADS),
+                     nseg * a * sizeof(float), stream, buf, ld, rows, a, nseg, off0, off1, g0, g1,
+                     inv_norm_dim, eps, rd);
   return hipGetLastError();
 }
 
