@@ -1,7 +1,10 @@
 // Bidirectional flash attention on MFMA for gfx950.
 //
-// Work split: one workgroup = 4 waves = 128 queries of one (sample, head);
-// a wave owns 32 queries and walks all keys in tiles of 64.
+// Work split: one workgroup = 4 waves of one (sample, head); a wave owns
+// QG groups of 32 queries and walks all keys in tiles of 64.  Each K and
+// V^T fragment read from LDS feeds the QG query groups, which halves LDS
+// read traffic per MFMA at QG = 2 (the LDS port, not the MFMA pipe, bounds
+// the one-group variant).
 //
 // The scores are computed transposed, S^T = K Q^T, with MFMA 32x32 tiles:
 // the A operand is the K tile (rows = keys, from LDS), the B operand is
@@ -18,17 +21,16 @@
 // with a lazy rescale: the exponent base only moves (and O^T, l are
 // rescaled) when a query's running max exceeds it by more than kSlack.
 // Key tails are masked to -inf; V^T chunks past the last key are zero-filled.
-// At most 256 registers per lane, so two waves share each SIMD and one
-// wave's softmax overlaps the other's MFMA work.
+// At QG = 1 the kernel fits in 256 registers per lane (two waves per SIMD);
+// at QG = 2 it runs one wave per SIMD with the accumulators in AGPRs.
 #include "common.h"
 #include "kernels.h"
 
 namespace dif {
 
-constexpr int AT_THREADS = 256;
-constexpr int AT_BM = 128;  // queries per workgroup
-constexpr int AT_BN = 64;   // keys per tile
-constexpr float kSlack = 8.f;  // log2 headroom of the lazy softmax rescale
+constexpr int AT_THREADS = 256;  // 4 waves
+constexpr int AT_BN = 64;        // keys per tile
+constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
 
 template <typename T>
 struct AttnParams {
@@ -47,8 +49,10 @@ __device__ __forceinline__ int key_slot(int kappa) {
   return 8 * k + 4 * gq + j;
 }
 
-template <typename T, int DH>
-__global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T> p) {
+// QG groups of 32 queries per wave: every K / V^T fragment read from LDS
+// feeds QG MFMAs.
+template <typename T, int DH, int QG>
+__global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel(AttnParams<T> p) {
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int KCH = DH * (int)sizeof(T) / 16;     // chunks per K row
   constexpr int VCH = AT_BN * (int)sizeof(T) / 16;  // chunks per V^T row
@@ -56,6 +60,7 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
   constexpr int NPC = 16 / VEC;                     // P chunks per 32-key sub-tile
   constexpr int K_PER_T = AT_BN * KCH / AT_THREADS;
   constexpr int V_PER_T = DH * VCH / AT_THREADS;
+  constexpr int BMQ = 4 * 32 * QG;                  // queries per workgroup
   static_assert(K_PER_T * AT_THREADS == AT_BN * KCH, "K tile split");
   static_assert(V_PER_T * AT_THREADS == DH * VCH, "V tile split");
   __shared__ u32x4 ks_[2][AT_BN][KCH];
@@ -64,19 +69,21 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int g = lane >> 5, col = lane & 31;
 
-  const int nqb = (p.Lq + AT_BM - 1) / AT_BM;
+  const int nqb = (p.Lq + BMQ - 1) / BMQ;
   const int bid = xcd_remap(blockIdx.x, nqb * p.H * p.B);
   const int qb = bid % nqb, hb = bid / nqb;
   const int h = hb % p.H, b = hb / p.H;
 
-  const int q = qb * AT_BM + wave * 32 + col;
-  const int64_t qrow = (int64_t)b * p.Lq + min(q, p.Lq - 1);
-
-  // Q^T fragments: chunk (2s + g) of this query's head slice
-  u32x4 qf[NQS];
+  // Q^T fragments: chunk (2s + g) of each of this lane's queries
+  u32x4 qf[QG][NQS];
 #pragma unroll
-  for (int s = 0; s < NQS; ++s)
-    qf[s] = *reinterpret_cast<const u32x4*>(p.Q + qrow * p.ldq + h * DH + (2 * s + g) * VEC);
+  for (int qg = 0; qg < QG; ++qg) {
+    const int q = qb * BMQ + (wave * QG + qg) * 32 + col;
+    const int64_t qrow = (int64_t)b * p.Lq + min(q, p.Lq - 1);
+#pragma unroll
+    for (int s = 0; s < NQS; ++s)
+      qf[qg][s] = *reinterpret_cast<const u32x4*>(p.Q + qrow * p.ldq + h * DH + (2 * s + g) * VEC);
+  }
 
   const T* kbase = p.K + (int64_t)b * p.Lk * p.ldk + h * DH;
   const T* vbase = p.Vt + ((int64_t)b * p.H + h) * DH * p.ldvt;
@@ -125,12 +132,19 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
     }
   };
 
-  f32x16 o[DH / 32];
+  f32x16 o[QG][DH / 32];
 #pragma unroll
-  for (int dt = 0; dt < DH / 32; ++dt)
+  for (int qg = 0; qg < QG; ++qg)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[qg][dt][r] = 0.f;
+  float m_run[QG], l_run[QG];
+#pragma unroll
+  for (int qg = 0; qg < QG; ++qg) {
+    m_run[qg] = -INFINITY;
+    l_run[qg] = 0.f;
+  }
 
   gload(0);
   sstore(0);
@@ -141,72 +155,74 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
     const bool more = kt + 1 < ntiles;
     if (more) gload(kt + 1);
 
-    // S^T for two 32-key sub-tiles
-    f32x16 s[2];
+    const int key0 = kt * AT_BN;
+    // the two 32-key halves of the tile in turn: S^T, softmax, O^T += V^T P^T
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
+      f32x16 s[QG];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[kk][r] = 0.f;
+      for (int qg = 0; qg < QG; ++qg)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[qg][r] = 0.f;
+      // every K fragment feeds the QG query groups
 #pragma unroll
       for (int st = 0; st < NQS; ++st) {
         const u32x4 a = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * st + g)];
-        Mma<T>::step(s[kk], a, qf[st]);
+#pragma unroll
+        for (int qg = 0; qg < QG; ++qg) Mma<T>::step(s[qg], a, qf[qg][st]);
       }
-    }
-    const int key0 = kt * AT_BN;
-    if (key0 + AT_BN > p.Lk) {
+      if (key0 + kk * 32 + 32 > p.Lk) {
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
+        for (int qg = 0; qg < QG; ++qg)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (key0 + kk * 32 + 16 * g + r >= p.Lk) s[kk][r] = -INFINITY;
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[kk][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * p.c;
-    // Lazy rescale: the exponent base m_run only moves when some query's
-    // max exceeds it by more than kSlack (probabilities stay <= 2^kSlack,
-    // far from float overflow); numerator and denominator share the base,
-    // so the normalised result is unchanged.
-    if (__any(mx > m_run + kSlack)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
-      m_run = m_new;
-    }
-    float rs = 0.f;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = __builtin_amdgcn_exp2f(fmaf(s[kk][r], p.c, -m_run));
-        s[kk][r] = e;
-        rs += e;
+          for (int r = 0; r < 16; ++r)
+            if (key0 + kk * 32 + 16 * g + r >= p.Lk) s[qg][r] = -INFINITY;
       }
-    rs += __shfl_xor(rs, 32);
-    l_run += rs;
-
-    // O^T += V^T P^T
+      u32x4 pc[QG][NPC];   // P^T chunks, packed as soon as they are computed
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
+      for (int qg = 0; qg < QG; ++qg) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[qg][r]);
+        mx *= p.c;
+        // Lazy rescale: the exponent base m_run (shared by the two lanes of
+        // a query) only moves when a score exceeds it by more than kSlack,
+        // so probabilities stay <= 2^kSlack; numerator and denominator share
+        // the base, so the normalised result is unchanged.  The cross-lane
+        // max is needed only then.  A fully masked sub-tile (mx = -inf)
+        // never moves the base.
+        if (__any(mx > m_run[qg] + kSlack)) {
+          mx = fmaxf(mx, __shfl_xor(mx, 32));
+          const float m_new = fmaxf(m_run[qg], mx);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[qg] - m_new);
+          l_run[qg] *= alpha;
+#pragma unroll
+          for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) o[qg][dt][r] *= alpha;
+          m_run[qg] = m_new;
+        }
+        // lane-partial row sum; the two lanes of a query are combined at the end
+#pragma unroll
+        for (int u = 0; u < NPC; ++u) {
+          float pv[VEC];
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            pv[e] = __builtin_amdgcn_exp2f(fmaf(s[qg][u * VEC + e], p.c, -m_run[qg]));
+            l_run[qg] += pv[e];
+          }
+          pc[qg][u] = Chunk<T>::pack(pv);
+        }
+      }
+      // every V^T fragment feeds the QG query groups
 #pragma unroll
       for (int u = 0; u < NPC; ++u) {
-        float pv[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) pv[e] = s[kk][u * VEC + e];
-        const u32x4 pc = Chunk<T>::pack(pv);
         const int vc = (kk * 32 + 16 * g) / VEC + u;
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) {
           const u32x4 a = vs_[buf][dt * 32 + col][swz<VCH>(col, vc)];
-          Mma<T>::step(o[dt], a, pc);
+#pragma unroll
+          for (int qg = 0; qg < QG; ++qg) Mma<T>::step(o[qg][dt], a, pc[qg][u]);
         }
       }
     }
@@ -215,8 +231,12 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
     __syncthreads();
   }
 
-  if (q < p.Lq) {
-    const float inv = 1.f / l_run;
+#pragma unroll
+  for (int qg = 0; qg < QG; ++qg) {
+    const int q = qb * BMQ + (wave * QG + qg) * 32 + col;
+    const float l = l_run[qg] + __shfl_xor(l_run[qg], 32);
+    if (q >= p.Lq) continue;
+    const float inv = 1.f / l;
     T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
 #pragma unroll
     for (int dt = 0; dt < DH / 32; ++dt)
@@ -226,16 +246,30 @@ __global__ __launch_bounds__(AT_THREADS, 2) void flash_attn_kernel(AttnParams<T>
         if constexpr (sizeof(T) == 4) {
           f32x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rr + e] * inv;
+          for (int e = 0; e < 4; ++e) v[e] = o[qg][dt][4 * rr + e] * inv;
           *reinterpret_cast<f32x4*>(dst + d) = v;
         } else {
           bf16x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[dt][4 * rr + e] * inv);
+          for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[qg][dt][4 * rr + e] * inv);
           *reinterpret_cast<bf16x4*>(dst + d) = v;
         }
       }
   }
+}
+
+#ifndef DIF_ATTN_QG
+#define DIF_ATTN_QG 1
+#endif
+
+template <typename T, int DH>
+void launch_dh(const AttnParams<T>& p, hipStream_t stream) {
+  // query groups per wave: one (two waves per SIMD hide the softmax behind
+  // the other wave's MFMAs better than the halved LDS traffic of two groups)
+  constexpr int QG = (sizeof(T) == 2 && DH == 128) ? DIF_ATTN_QG : 1;
+  constexpr int BMQ = 4 * 32 * QG;
+  const int blocks = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
+  hipLaunchKernelGGL((flash_attn_kernel<T, DH, QG>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
 }
 
 template <typename T>
@@ -245,12 +279,10 @@ hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, i
   if (B <= 0 || Lq <= 0 || H <= 0) return hipSuccess;
   AttnParams<T> p{Q, K, Vt, O, ldq, ldk, ldvt, ldo, B, Lq, Lk, H,
                   1.4426950408889634f / sqrtf((float)head_dim)};
-  const int blocks = ((Lq + AT_BM - 1) / AT_BM) * H * B;
-  dim3 grid(blocks), block(AT_THREADS);
   if (head_dim == 128) {
-    hipLaunchKernelGGL((flash_attn_kernel<T, 128>), grid, block, 0, stream, p);
+    launch_dh<T, 128>(p, stream);
   } else if (head_dim == 64) {
-    hipLaunchKernelGGL((flash_attn_kernel<T, 64>), grid, block, 0, stream, p);
+    launch_dh<T, 64>(p, stream);
   } else {
     return hipErrorInvalidValue;
   }

@@ -127,13 +127,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
         for (int j = 0; j < TN; ++j) Mma<T>::step(acc[i][j], af[i], bfr[j]);
     }
   };
-  // one k-tile: `cur` holds the tile after kt (stored at the end), `nxt`
-  // receives tile kt + 2
+  // one k-tile: after the barrier tile kt is visible and buffer (kt+1)&1 is
+  // free; `cur` holds tile kt+1 (stored first), `nxt` receives tile kt+2
   auto ktile = [&](int kt, u32x4* ra_cur, u32x4* rb_cur, u32x4* ra_nxt, u32x4* rb_nxt) {
+    __syncthreads();
+    if (kt + 1 < nk) sstore((kt + 1) & 1, ra_cur, rb_cur);
     if (kt + 2 < nk) gload(kt + 2, ra_nxt, rb_nxt);
     compute(kt & 1);
-    if (kt + 1 < nk) sstore((kt + 1) & 1, ra_cur, rb_cur);
-    __syncthreads();
   };
 
   if (nk > 0) {
@@ -141,13 +141,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
     sstore(0, ra0, rb0);
     if (nk > 1) gload(1, ra1, rb1);
   }
-  __syncthreads();
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
     ktile(kt, ra1, rb1, ra0, rb0);       // tile kt+1 is in set 1, kt+2 goes to set 0
     ktile(kt + 1, ra0, rb0, ra1, rb1);   // tile kt+2 is in set 0, kt+3 goes to set 1
   }
   if (kt < nk) ktile(kt, ra1, rb1, ra0, rb0);
+  __syncthreads();
 
   // epilogue: lane holds column n of each tile, 16 rows
 #pragma unroll
