@@ -1,0 +1,97 @@
+"""Full-size parity: one block at the benchmark's shapes, on sampled rows.
+
+The GPU runs the whole block (all L tokens, the launch configuration the
+benchmark times); the oracle computes the same block for a sample of query
+rows, with keys and values of self-attention over all L tokens.  Samples
+include the first rows and the ragged tail (L = 32760 = 127 * 256 + 248,
+75600 = 295 * 256 + 80).  The oracle runs in float32 here to keep the
+masked-dense projections (up to 8 TFLOP) within seconds; float32 vs float64
+differs by ~1e-6, far below the bf16 tolerance 2e-2.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_06631_amd import binding as B
+from tests.gpu_util import make_model, rel_err, say, to_dev, to_np
+from workloads import get_config, synth
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+TOL = 2e-2
+
+
+def _rows(L, seed, n=160):
+    g = np.random.default_rng(seed)
+    return np.unique(np.concatenate([np.arange(24), g.choice(L, n, replace=False),
+                                     np.arange(L - 40, L)]))
+
+
+def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False):
+    import torch
+    one = cfg.with_(n_layers=1)
+    m1 = {k: v[layer:layer + 1] for k, v in masks.items()}
+    say(f"{cfg.name}: L={cfg.seq_len} layer={layer} heads={int(m1['self_head_keep'].sum())} "
+        f"cross={int(m1['cross_head_keep'].sum())} ffn={int(m1['ffn_keep'].sum())} "
+        f"{'ffn-gate-off ' if gate_ffn_off else ''}seed={seed}")
+    x = synth.make_block_input(one, seed, scale=x_scale)
+    ctx = synth.make_context(one, seed)
+    e0 = synth.make_e0(one, seed, std=0.3)
+    if gate_ffn_off:
+        e0[5] = -wl["mod"][5]
+    w = synth.make_global_weights(one, 0)
+    w["layers"] = [wl]
+    model = make_model(one, w)
+    plan = B.dif_plan_step(model, 0, m1)
+    xd, cd = to_dev(x, one), to_dev(ctx, one)
+    ed = to_dev(e0, dtype=torch.float32)
+    ws = B.workspace(model, 1, one.seq_len, one.text_len)
+    B.dif_block_forward(plan, 0, xd, cd, ed, ws)
+    torch.cuda.synchronize()
+    got = to_np(xd)[0]
+    say("  GPU block done; oracle on sampled rows")
+    rows = _rows(one.seq_len, seed)
+    wz = O.apply_keep(wl, m1["self_head_keep"][0], m1["cross_head_keep"][0], m1["ffn_keep"][0],
+                      one.head_dim, np.float32)
+    ref = O.block(x[0], ctx[0], e0, wz, True, one.n_heads, one.head_dim, one.grid, one.rope_theta,
+                  one.eps, rows=rows, dtype=np.float32)
+    err = rel_err(got[rows], ref)
+    say(f"  rel err {err:.3e} over {len(rows)} rows")
+    assert err <= TOL
+
+
+@pytest.fixture(scope="module")
+def c3_layer():
+    cfg = get_config("wan14b_block")
+    say("generating one Wan-14B-shaped layer")
+    return cfg, synth.make_layer_weights(cfg, 0, 0)
+
+
+def test_wan13b_block_fullsize():
+    cfg = get_config("wan1.3b_block")
+    wl = synth.make_layer_weights(cfg, 0, 0)
+    masks = synth.make_masks(cfg, 0)
+    _check(cfg, wl, masks, 0, seed=31)
+    _check(cfg, wl, masks, 0, seed=32, gate_ffn_off=True)
+
+
+@pytest.mark.parametrize("step", [0, 1, 2, 3])
+def test_wan14b_block_fullsize_each_structure(c3_layer, step):
+    cfg, wl = c3_layer
+    _check(cfg, wl, synth.make_masks(cfg, step), 0, seed=40 + step, gate_ffn_off=(step == 3))
+
+
+def test_wan14b_480p_stack_layer_recipe_masks():
+    """A deep layer of the 40-layer stack under the depth-tilted recipe at t3."""
+    cfg = get_config("wan14b_480p")
+    masks = synth.make_masks(cfg, 2)
+    layer = 33
+    wl = synth.make_layer_weights(cfg, layer, 0)
+    _check(cfg, wl, masks, layer, seed=50)
+
+
+def test_wan14b_720p_block_fullsize():
+    cfg = get_config("wan14b_720p")
+    masks = synth.make_masks(cfg, 1)
+    wl = synth.make_layer_weights(cfg, 0, 0)
+    _check(cfg, wl, masks, 0, seed=60, gate_ffn_off=True)
