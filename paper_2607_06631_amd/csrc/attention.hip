@@ -89,30 +89,58 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
   const T* vbase = p.Vt + ((int64_t)b * p.H + h) * DH * p.ldvt;
   const int ntiles = (p.Lk + AT_BN - 1) / AT_BN;
 
+  // Tile loads are buffer loads: per-tile descriptors are built in SGPRs
+  // and every lane's offset is tile-invariant.  K rows at or past Lk fall
+  // outside the K descriptor and read as zero (their scores are masked);
+  // a tile that ends past Lk takes the per-element path for V^T.
+  constexpr uint32_t kRsrcWord3 = 0x00020000u;
+  constexpr int ES = (int)sizeof(T);
+  uint32_t k_off[K_PER_T], v_off[V_PER_T];
+#pragma unroll
+  for (int i = 0; i < K_PER_T; ++i) {
+    const int id = tid + AT_THREADS * i;
+    k_off[i] = (uint32_t)(((id / KCH) * p.ldk + (id % KCH) * VEC) * ES);
+  }
+#pragma unroll
+  for (int i = 0; i < V_PER_T; ++i) {
+    const int id = tid + AT_THREADS * i;
+    v_off[i] = (uint32_t)(((id / VCH) * p.ldvt + (id % VCH) * VEC) * ES);
+  }
+  const int64_t v_bytes = (int64_t)DH * p.ldvt * ES;
+
   u32x4 kreg[K_PER_T], vreg[V_PER_T];
   auto gload = [&](int kt) {
     const int key0 = kt * AT_BN;
+    const int64_t kb = (int64_t)(p.Lk - key0) * p.ldk * ES;
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(kbase + (int64_t)key0 * p.ldk), (short)0,
+        (uint32_t)(kb < 0xffffffffll ? kb : 0xffffffffll), kRsrcWord3);
 #pragma unroll
-    for (int i = 0; i < K_PER_T; ++i) {
-      const int id = tid + AT_THREADS * i;
-      const int key = min(key0 + id / KCH, p.Lk - 1);
-      kreg[i] = *reinterpret_cast<const u32x4*>(kbase + (int64_t)key * p.ldk + (id % KCH) * VEC);
-    }
+    for (int i = 0; i < K_PER_T; ++i)
+      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, k_off[i], 0, 0));
+    if (key0 + AT_BN <= p.Lk) {
+      const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
 #pragma unroll
-    for (int i = 0; i < V_PER_T; ++i) {
-      const int id = tid + AT_THREADS * i;
-      const int d = id / VCH, k0 = key0 + (id % VCH) * VEC;
-      if (k0 + VEC <= p.Lk) {
-        vreg[i] = *reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0);
-      } else if (k0 < p.Lk) {
-        float tmp[VEC];
-        Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0), tmp);
+      for (int i = 0; i < V_PER_T; ++i)
+        vreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, v_off[i], 0, 0));
+    } else {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e)
-          if (k0 + e >= p.Lk) tmp[e] = 0.f;
-        vreg[i] = Chunk<T>::pack(tmp);
-      } else {
-        vreg[i] = u32x4{0u, 0u, 0u, 0u};
+      for (int i = 0; i < V_PER_T; ++i) {
+        const int id = tid + AT_THREADS * i;
+        const int d = id / VCH, k0 = key0 + (id % VCH) * VEC;
+        if (k0 + VEC <= p.Lk) {
+          vreg[i] = *reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0);
+        } else if (k0 < p.Lk) {
+          float tmp[VEC];
+          Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0), tmp);
+#pragma unroll
+          for (int e = 0; e < VEC; ++e)
+            if (k0 + e >= p.Lk) tmp[e] = 0.f;
+          vreg[i] = Chunk<T>::pack(tmp);
+        } else {
+          vreg[i] = u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
   };
