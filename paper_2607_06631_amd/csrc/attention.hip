@@ -89,75 +89,90 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
   const T* vbase = p.Vt + ((int64_t)b * p.H + h) * DH * p.ldvt;
   const int ntiles = (p.Lk + AT_BN - 1) / AT_BN;
 
-  // Tile loads are buffer loads: per-tile descriptors are built in SGPRs
-  // and every lane's offset is tile-invariant.  K rows at or past Lk fall
-  // outside the K descriptor and read as zero (their scores are masked);
-  // a tile that ends past Lk takes the per-element path for V^T.
+  // Full tiles are copied straight into LDS with buffer loads (no staging
+  // registers): each wave instruction fills 1 KB of LDS, lane l writing
+  // bytes [16 l, 16 l + 16), so every lane fetches the element that the
+  // permuted / swizzled layout puts in its slot.  Per-tile descriptors are
+  // built in SGPRs and lane offsets are tile-invariant.  K rows at or past
+  // Lk fall outside the K descriptor and read as zero (their scores are
+  // masked).  The last tile, if it ends past Lk, goes through registers and
+  // zero-fills V^T beyond Lk element by element.
   constexpr uint32_t kRsrcWord3 = 0x00020000u;
   constexpr int ES = (int)sizeof(T);
-  uint32_t k_off[K_PER_T], v_off[V_PER_T];
+  constexpr int KRPI = 64 / KCH;                  // K rows per wave instruction
+  constexpr int VRPI = 64 / VCH;                  // V^T rows per wave instruction
+  constexpr int KI = AT_BN / (KRPI * 4);          // K instructions per wave
+  constexpr int VI = DH / (VRPI * 4);             // V^T instructions per wave
+  static_assert(KI * KRPI * 4 == AT_BN && VI * VRPI * 4 == DH, "direct tile split");
+  uint32_t kd_off[KI], vd_off[VI];
 #pragma unroll
-  for (int i = 0; i < K_PER_T; ++i) {
-    const int id = tid + AT_THREADS * i;
-    k_off[i] = (uint32_t)(((id / KCH) * p.ldk + (id % KCH) * VEC) * ES);
+  for (int j = 0; j < KI; ++j) {
+    const int row = (j * 4 + wave) * KRPI + lane / KCH;        // LDS row
+    const int kk = row >> 5, i = row & 31;
+    const int key = kk * 32 + 16 * ((i >> 2) & 1) + 4 * (i >> 3) + (i & 3);  // inverse of key_slot
+    kd_off[j] = (uint32_t)((key * p.ldk + swz<KCH>(row, lane % KCH) * VEC) * ES);
   }
 #pragma unroll
-  for (int i = 0; i < V_PER_T; ++i) {
-    const int id = tid + AT_THREADS * i;
-    v_off[i] = (uint32_t)(((id / VCH) * p.ldvt + (id % VCH) * VEC) * ES);
+  for (int j = 0; j < VI; ++j) {
+    const int d = (j * 4 + wave) * VRPI + lane / VCH;
+    vd_off[j] = (uint32_t)((d * p.ldvt + swz<VCH>(d, lane % VCH) * VEC) * ES);
   }
   const int64_t v_bytes = (int64_t)DH * p.ldvt * ES;
-
-  u32x4 kreg[K_PER_T], vreg[V_PER_T];
-  auto gload = [&](int kt) {
-    const int key0 = kt * AT_BN;
+  auto k_rsrc = [&](int key0) {
     const int64_t kb = (int64_t)(p.Lk - key0) * p.ldk * ES;
-    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
-        const_cast<T*>(kbase + (int64_t)key0 * p.ldk), (short)0,
-        (uint32_t)(kb < 0xffffffffll ? kb : 0xffffffffll), kRsrcWord3);
-#pragma unroll
-    for (int i = 0; i < K_PER_T; ++i)
-      kreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, k_off[i], 0, 0));
-    if (key0 + AT_BN <= p.Lk) {
-      const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
-#pragma unroll
-      for (int i = 0; i < V_PER_T; ++i)
-        vreg[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(vr, v_off[i], 0, 0));
-    } else {
-#pragma unroll
-      for (int i = 0; i < V_PER_T; ++i) {
-        const int id = tid + AT_THREADS * i;
-        const int d = id / VCH, k0 = key0 + (id % VCH) * VEC;
-        if (k0 + VEC <= p.Lk) {
-          vreg[i] = *reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0);
-        } else if (k0 < p.Lk) {
-          float tmp[VEC];
-          Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0), tmp);
-#pragma unroll
-          for (int e = 0; e < VEC; ++e)
-            if (k0 + e >= p.Lk) tmp[e] = 0.f;
-          vreg[i] = Chunk<T>::pack(tmp);
-        } else {
-          vreg[i] = u32x4{0u, 0u, 0u, 0u};
-        }
-      }
-    }
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kbase + (int64_t)key0 * p.ldk), (short)0,
+                                             (uint32_t)(kb < 0xffffffffll ? kb : 0xffffffffll),
+                                             kRsrcWord3);
   };
-  auto sstore = [&](int buf) {
+  auto load_direct = [&](int kt, int buf) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    typedef __attribute__((address_space(3))) void lds_t;
+    const int key0 = kt * AT_BN;
+    const __amdgpu_buffer_rsrc_t kr = k_rsrc(key0);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
+#pragma unroll
+    for (int j = 0; j < KI; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_t*)&ks_[buf][(j * 4 + wave) * KRPI][0], 16,
+                                               kd_off[j], 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < VI; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vs_[buf][(j * 4 + wave) * VRPI][0], 16,
+                                               vd_off[j], 0, 0, 0);
+#endif
+  };
+  // tail tile: through registers, V^T zero-filled past Lk
+  auto load_tail = [&](int kt, int buf) {
+    const int key0 = kt * AT_BN;
+    const __amdgpu_buffer_rsrc_t kr = k_rsrc(key0);
 #pragma unroll
     for (int i = 0; i < K_PER_T; ++i) {
       const int id = tid + AT_THREADS * i;
       const int kl = id / KCH, c = id % KCH;
+      const u32x4 v = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)((kl * p.ldk + c * VEC) * ES), 0, 0));
       const int row = (kl & ~31) + key_slot(kl & 31);
-      ks_[buf][row][swz<KCH>(row, c)] = kreg[i];
+      ks_[buf][row][swz<KCH>(row, c)] = v;
     }
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
       const int id = tid + AT_THREADS * i;
-      const int d = id / VCH, c = id % VCH;
-      vs_[buf][d][swz<VCH>(d, c)] = vreg[i];
+      const int d = id / VCH, c = id % VCH, k0 = key0 + c * VEC;
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (k0 < p.Lk) {
+        float tmp[VEC];
+        Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0), tmp);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (k0 + e >= p.Lk) tmp[e] = 0.f;
+        v = Chunk<T>::pack(tmp);
+      }
+      vs_[buf][d][swz<VCH>(d, c)] = v;
     }
+  };
+  auto load_tile = [&](int kt, int buf) {
+    if ((kt + 1) * AT_BN <= p.Lk) load_direct(kt, buf);
+    else load_tail(kt, buf);
   };
 
   f32x16 o[QG][DH / 32];
@@ -174,14 +189,14 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
     l_run[qg] = 0.f;
   }
 
-  gload(0);
-  sstore(0);
-  __syncthreads();
+  load_tile(0, 0);
+  wait_vmcnt<0>();   // this wave's direct-to-LDS loads have landed
+  __syncthreads();   // ... and every other wave's
 
   for (int kt = 0; kt < ntiles; ++kt) {
     const int buf = kt & 1;
-    const bool more = kt + 1 < ntiles;
-    if (more) gload(kt + 1);
+    // buffer buf^1 was last read before the previous barrier
+    if (kt + 1 < ntiles) load_tile(kt + 1, buf ^ 1);
 
     const int key0 = kt * AT_BN;
     // the two 32-key halves of the tile in turn: S^T, softmax, O^T += V^T P^T
@@ -255,7 +270,7 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
       }
     }
 
-    if (more) sstore(buf ^ 1);
+    wait_vmcnt<0>();   // tile kt+1 (direct-to-LDS) has landed for this wave
     __syncthreads();
   }
 

@@ -104,6 +104,15 @@ __device__ __forceinline__ int swz(int row, int c) {
   }
 }
 
+// s_waitcnt vmcnt(n) with the other counters left alone.  Buffer loads
+// that write LDS directly are counted by vmcnt, and a workgroup barrier
+// does not wait for them on its own.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
