@@ -28,7 +28,11 @@
 
 namespace dif {
 
-constexpr int AT_THREADS = 256;  // 4 waves
+#ifndef DIF_ATTN_WAVES
+#define DIF_ATTN_WAVES 4
+#endif
+constexpr int AT_WAVES = DIF_ATTN_WAVES;
+constexpr int AT_THREADS = 64 * AT_WAVES;
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
 
@@ -52,7 +56,7 @@ __device__ __forceinline__ int key_slot(int kappa) {
 // QG groups of 32 queries per wave: every K / V^T fragment read from LDS
 // feeds QG MFMAs.
 template <typename T, int DH, int QG>
-__global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel(AttnParams<T> p) {
+__global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_attn_kernel(AttnParams<T> p) {
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int KCH = DH * (int)sizeof(T) / 16;     // chunks per K row
   constexpr int VCH = AT_BN * (int)sizeof(T) / 16;  // chunks per V^T row
@@ -60,7 +64,7 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
   constexpr int NPC = 16 / VEC;                     // P chunks per 32-key sub-tile
   constexpr int K_PER_T = AT_BN * KCH / AT_THREADS;
   constexpr int V_PER_T = DH * VCH / AT_THREADS;
-  constexpr int BMQ = 4 * 32 * QG;                  // queries per workgroup
+  constexpr int BMQ = AT_WAVES * 32 * QG;           // queries per workgroup
   static_assert(K_PER_T * AT_THREADS == AT_BN * KCH, "K tile split");
   static_assert(V_PER_T * AT_THREADS == DH * VCH, "V tile split");
   __shared__ u32x4 ks_[2][AT_BN][KCH];
@@ -101,20 +105,20 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
   constexpr int ES = (int)sizeof(T);
   constexpr int KRPI = 64 / KCH;                  // K rows per wave instruction
   constexpr int VRPI = 64 / VCH;                  // V^T rows per wave instruction
-  constexpr int KI = AT_BN / (KRPI * 4);          // K instructions per wave
-  constexpr int VI = DH / (VRPI * 4);             // V^T instructions per wave
-  static_assert(KI * KRPI * 4 == AT_BN && VI * VRPI * 4 == DH, "direct tile split");
+  constexpr int KI = AT_BN / (KRPI * AT_WAVES);   // K instructions per wave
+  constexpr int VI = DH / (VRPI * AT_WAVES);      // V^T instructions per wave
+  static_assert(KI * KRPI * AT_WAVES == AT_BN && VI * VRPI * AT_WAVES == DH, "direct tile split");
   uint32_t kd_off[KI], vd_off[VI];
 #pragma unroll
   for (int j = 0; j < KI; ++j) {
-    const int row = (j * 4 + wave) * KRPI + lane / KCH;        // LDS row
+    const int row = (j * AT_WAVES + wave) * KRPI + lane / KCH;  // LDS row
     const int kk = row >> 5, i = row & 31;
     const int key = kk * 32 + 16 * ((i >> 2) & 1) + 4 * (i >> 3) + (i & 3);  // inverse of key_slot
     kd_off[j] = (uint32_t)((key * p.ldk + swz<KCH>(row, lane % KCH) * VEC) * ES);
   }
 #pragma unroll
   for (int j = 0; j < VI; ++j) {
-    const int d = (j * 4 + wave) * VRPI + lane / VCH;
+    const int d = (j * AT_WAVES + wave) * VRPI + lane / VCH;
     vd_off[j] = (uint32_t)((d * p.ldvt + swz<VCH>(d, lane % VCH) * VEC) * ES);
   }
   const int64_t v_bytes = (int64_t)DH * p.ldvt * ES;
@@ -133,11 +137,11 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
         const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
 #pragma unroll
     for (int j = 0; j < KI; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_t*)&ks_[buf][(j * 4 + wave) * KRPI][0], 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_t*)&ks_[buf][(j * AT_WAVES + wave) * KRPI][0], 16,
                                                kd_off[j], 0, 0, 0);
 #pragma unroll
     for (int j = 0; j < VI; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vs_[buf][(j * 4 + wave) * VRPI][0], 16,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vs_[buf][(j * AT_WAVES + wave) * VRPI][0], 16,
                                                vd_off[j], 0, 0, 0);
 #endif
   };
@@ -207,13 +211,24 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
       for (int qg = 0; qg < QG; ++qg)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[qg][r] = 0.f;
-      // every K fragment feeds the QG query groups
+      // every K fragment feeds the QG query groups; all of the half's
+      // fragment reads are issued before its MFMAs
+      u32x4 kf[NQS];
 #pragma unroll
-      for (int st = 0; st < NQS; ++st) {
-        const u32x4 a = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * st + g)];
+      for (int st = 0; st < NQS; ++st) kf[st] = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * st + g)];
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int qg = 0; qg < QG; ++qg) Mma<T>::step(s[qg], a, qf[qg][st]);
-      }
+      for (int st = 0; st < NQS; ++st)
+#pragma unroll
+        for (int qg = 0; qg < QG; ++qg) Mma<T>::step(s[qg], kf[st], qf[qg][st]);
+      // V^T fragments of this half, in flight during the softmax
+      u32x4 vf[NPC][DH / 32];
+#pragma unroll
+      for (int u = 0; u < NPC; ++u)
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; ++dt)
+          vf[u][dt] = vs_[buf][dt * 32 + col][swz<VCH>(col, (kk * 32 + 16 * g) / VEC + u)];
+      __builtin_amdgcn_sched_barrier(0);
       if (key0 + kk * 32 + 32 > p.Lk) {
 #pragma unroll
         for (int qg = 0; qg < QG; ++qg)
@@ -259,15 +274,11 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 2 : 1) void flash_attn_kernel
       }
       // every V^T fragment feeds the QG query groups
 #pragma unroll
-      for (int u = 0; u < NPC; ++u) {
-        const int vc = (kk * 32 + 16 * g) / VEC + u;
+      for (int u = 0; u < NPC; ++u)
 #pragma unroll
-        for (int dt = 0; dt < DH / 32; ++dt) {
-          const u32x4 a = vs_[buf][dt * 32 + col][swz<VCH>(col, vc)];
+        for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-          for (int qg = 0; qg < QG; ++qg) Mma<T>::step(o[qg][dt], a, pc[qg][u]);
-        }
-      }
+          for (int qg = 0; qg < QG; ++qg) Mma<T>::step(o[qg][dt], vf[u][dt], pc[qg][u]);
     }
 
     wait_vmcnt<0>();   // tile kt+1 (direct-to-LDS) has landed for this wave
@@ -310,7 +321,7 @@ void launch_dh(const AttnParams<T>& p, hipStream_t stream) {
   // query groups per wave: one (two waves per SIMD hide the softmax behind
   // the other wave's MFMAs better than the halved LDS traffic of two groups)
   constexpr int QG = (sizeof(T) == 2 && DH == 128) ? DIF_ATTN_QG : 1;
-  constexpr int BMQ = 4 * 32 * QG;
+  constexpr int BMQ = AT_WAVES * 32 * QG;
   const int blocks = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
   hipLaunchKernelGGL((flash_attn_kernel<T, DH, QG>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
 }
