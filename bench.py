@@ -55,6 +55,9 @@ def parse():
                     help="time the steps without per-kernel events")
     ap.add_argument("--cpu-tokens", type=int, default=0,
                     help="token count of the CPU oracle sample (0: auto)")
+    ap.add_argument("--plan", default="compact", choices=["compact", "indexed"],
+                    help="compact: per-step gathered weights; indexed: union weights read "
+                         "in place through the index tables")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before the steps, run one plain device copy of this many MiB "
                          "(the reference dispatch that scales HBM byte counters)")
@@ -154,7 +157,8 @@ def main():
     log(f"bench: weights ready ({time.perf_counter() - t_setup:.1f} s)")
     model = B.dif_model_create(cfg, w)
     masks = [synth.make_masks(cfg, s) for s in range(4)]
-    plans = [B.dif_plan_step(model, s, masks[s]) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, masks[s], kind=args.plan) for s in range(4)]
+    plan_bytes = sum(p.mem.numel() for p in plans)
     gen = torch.Generator(device=dev)
     gen.manual_seed(1)
     z = torch.randn((1, L, cfg.patch_dim), generator=gen, device=dev, dtype=torch.float32)
@@ -273,7 +277,8 @@ def main():
                                 f"{L} video tokens ({'x'.join(map(str, cfg.grid))}), {Lc} text "
                                 f"tokens, batch 1, 4 step structures"),
                    "layers": N, "seq_len": L, "text_len": Lc, "dim": D, "heads": H,
-                   "ffn": F, "parallelism": "none (1 GPU)"},
+                   "ffn": F, "parallelism": "none (1 GPU)", "plan": args.plan},
+        "plan_gb_4_structures": round(plan_bytes / 1e9, 3),
         "effective_tflops": round(tflops, 1),
         "frac_mfma_peak": round(tflops / peak, 4),
         "kept_tflop_per_step": [round(f / 1e12, 2) for f in step_flops],

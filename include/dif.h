@@ -125,8 +125,14 @@ typedef struct dif_layer_info {
   int32_t self_heads;   /* h   */
   int32_t cross_heads;  /* h_c */
   int32_t ffn_channels; /* f   */
-  int32_t ffn_padded;   /* f rounded up to 64: width of the compacted FFN */
+  int32_t ffn_padded;   /* FFN width the GEMMs run: compact plans f rounded up
+                           to 64; indexed plans 16-byte channel chunks holding
+                           a kept channel, rounded up to 64 */
 } dif_layer_info;
+
+/* How a plan presents step t's active parameters to the kernels. */
+#define DIF_PLAN_COMPACT 0 /* gathered once into contiguous per-step weights */
+#define DIF_PLAN_INDEXED 1 /* read in place from theta_union through I_t    */
 
 typedef struct dif_model dif_model;
 typedef struct dif_plan dif_plan;
@@ -163,6 +169,29 @@ dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, s
  * DIF_E_HIP. */
 dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_masks* masks,
                          void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out);
+
+/* Plan of either kind (DIF_PLAN_COMPACT is dif_plan_bytes / dif_plan_step).
+ *
+ * DIF_PLAN_INDEXED keeps only theta_union and the index tables I_t, as the
+ * paper's inference engine does (Sec. 4.3, Fig. 2(c)): the GEMMs gather
+ * kept q/k/v, cross-q/k/v and W1 rows (and their biases and QK-norm gains)
+ * by row index, and read the kept columns of Wo, cross-Wo and W2 as
+ * 16-byte chunks through a chunk table, so no weight is copied and plan
+ * memory is the tables plus the RoPE table (kilobytes per layer).  FFN
+ * channels are taken in chunks of 16 bytes (8 bf16 / 4 float32 channels,
+ * the paper's C = 8 chunks at bf16; App. A): a chunk with any kept channel
+ * is run whole with its dropped channels zeroed, so the result equals the
+ * compact plan's (exactly, when every chunk is wholly kept or dropped, as
+ * with C = 8 gates).  Requires ffn_dim % 8 == 0 and ffn_dim <= 65536
+ * (bf16) / 32768 (float32), else DIF_E_UNSUPPORTED.  The union weights
+ * must stay valid and unchanged while the plan is used.  Other arguments,
+ * ownership and errors as dif_plan_step; an unknown kind is DIF_E_ARG. */
+dif_status dif_plan_bytes_ex(const dif_model* model, const dif_step_masks* masks, int32_t kind,
+                             size_t* bytes);
+dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step_masks* masks,
+                            int32_t kind, void* plan_mem, size_t plan_bytes, dif_stream stream,
+                            dif_plan** out);
+
 /* Frees the plan's host metadata only (plan_mem stays the caller's).  The
  * caller must synchronise `stream` before freeing plan_mem. */
 dif_status dif_plan_destroy(dif_plan* plan);

@@ -84,6 +84,9 @@ def lib():
             "dif_model_destroy": (i32, [vp]),
             "dif_plan_bytes": (i32, [vp, C.POINTER(DifStepMasks), C.POINTER(sz)]),
             "dif_plan_step": (i32, [vp, i32, C.POINTER(DifStepMasks), vp, sz, vp, C.POINTER(vp)]),
+            "dif_plan_bytes_ex": (i32, [vp, C.POINTER(DifStepMasks), i32, C.POINTER(sz)]),
+            "dif_plan_step_ex": (i32, [vp, i32, C.POINTER(DifStepMasks), i32, vp, sz, vp,
+                                       C.POINTER(vp)]),
             "dif_plan_destroy": (i32, [vp]),
             "dif_plan_layer_info": (i32, [vp, i32, C.POINTER(DifLayerInfo)]),
             "dif_workspace_bytes": (i32, [vp, i32, i32, i32, C.POINTER(sz)]),
@@ -234,25 +237,33 @@ def dif_model_create(cfg, weights: Dict) -> Model:
     return Model(cfg, weights)
 
 
-def dif_plan_bytes(model: Model, masks) -> int:
+DIF_PLAN_COMPACT, DIF_PLAN_INDEXED = 0, 1
+PLAN_KINDS = {"compact": DIF_PLAN_COMPACT, "indexed": DIF_PLAN_INDEXED}
+
+
+def dif_plan_bytes(model: Model, masks, kind: str = "compact") -> int:
     m = _Masks(masks)
     n = C.c_size_t()
-    _check(lib().dif_plan_bytes(model.handle, C.byref(m.struct), C.byref(n)))
+    _check(lib().dif_plan_bytes_ex(model.handle, C.byref(m.struct), PLAN_KINDS[kind], C.byref(n)))
     return n.value
 
 
-def dif_plan_step(model: Model, step: int, masks, stream=None) -> Plan:
-    """Index tables + gather of the step's active parameters into plan memory
-    allocated here with torch (owned by the returned Plan)."""
+def dif_plan_step(model: Model, step: int, masks, stream=None, kind: str = "compact") -> Plan:
+    """Index tables (and, for kind="compact", the gather of the step's active
+    parameters) in plan memory allocated here with torch (owned by the
+    returned Plan)."""
     import torch
     m = _Masks(masks)
     n = C.c_size_t()
-    _check(lib().dif_plan_bytes(model.handle, C.byref(m.struct), C.byref(n)))
+    k = PLAN_KINDS[kind]
+    _check(lib().dif_plan_bytes_ex(model.handle, C.byref(m.struct), k, C.byref(n)))
     mem = torch.empty(max(n.value, 256), dtype=torch.uint8, device="cuda")
     h = C.c_void_p()
-    _check(lib().dif_plan_step(model.handle, step, C.byref(m.struct), mem.data_ptr(), n.value,
-                               _stream(stream), C.byref(h)))
-    return Plan(model, h, mem, m, step)
+    _check(lib().dif_plan_step_ex(model.handle, step, C.byref(m.struct), k, mem.data_ptr(), n.value,
+                                  _stream(stream), C.byref(h)))
+    plan = Plan(model, h, mem, m, step)
+    plan.kind = kind
+    return plan
 
 
 def dif_workspace_bytes(model: Model, B: int, L: int, Lc: int) -> int:

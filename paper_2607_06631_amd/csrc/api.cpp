@@ -148,6 +148,20 @@ dif_status check_config(const dif_config* c) {
   return DIF_OK;
 }
 
+// Indexed plans read 16-byte chunks of W2's rows in place: the FFN width
+// must be whole chunks for either dtype, and one layer's chunk table must
+// fit the GEMM's LDS table (8192 chunks).
+dif_status check_plan_kind(const dif_config* c, int32_t kind) {
+  if (kind == DIF_PLAN_COMPACT) return DIF_OK;
+  if (kind != DIF_PLAN_INDEXED) return fail(DIF_E_ARG, "unknown plan kind %d", kind);
+  if (c->ffn_dim % 8 != 0)
+    return fail(DIF_E_UNSUPPORTED, "indexed plan: ffn_dim %d must be a multiple of 8", c->ffn_dim);
+  const int vec = (int)(16 / esize(c->dtype));
+  if ((int64_t)round_up(c->ffn_dim, 64) / vec > 8192)
+    return fail(DIF_E_UNSUPPORTED, "indexed plan: ffn_dim %d too large", c->ffn_dim);
+  return DIF_OK;
+}
+
 dif_status check_masks(const dif_config* c, const dif_step_masks* m) {
   if (!m || !m->block_keep || !m->self_head_keep || !m->cross_head_keep || !m->ffn_keep)
     return fail(DIF_E_MASK, "mask pointer is null");
@@ -178,11 +192,15 @@ struct LayerPlan {
   size_t o_w1 = 0, o_b1 = 0, o_w2 = 0;
   size_t o_idx_self = 0, o_idx_cross = 0, o_idx_ffn = 0;   // device index tables
   size_t h_idx_self = 0, h_idx_cross = 0, h_idx_ffn = 0;   // offsets into host_idx
+  // indexed plans: K-chunk tables (16-byte chunks of the union's reduction axis)
+  size_t o_kch_self = 0, o_kch_cross = 0, o_kch_ffn = 0;
+  size_t h_kch_self = 0, h_kch_cross = 0, h_kch_ffn = 0;
   char* base = nullptr;
   template <typename P> P* at(size_t off) const { return reinterpret_cast<P*>(base + off); }
 };
 
 struct Layout {
+  bool indexed = false;
   std::vector<LayerPlan> layers;
   std::vector<int32_t> host_idx;
   size_t o_rope = 0, n_rope = 0, o_idx = 0, total = 0;
@@ -224,48 +242,93 @@ struct dif_plan {
 
 namespace {
 
-Layout build_layout(const dif_model* m, const dif_step_masks* mk) {
+// Index tables of one step structure (Sec. 4.3, I_t).
+//   compact plan: kept rows (heads: h*dh entries; FFN: kept channels, -1 up
+//     to the 64-padded width), then the compacted weights carved after them.
+//   indexed plan: the same head row tables plus, per table, the 16-byte
+//     chunks of the union's reduction axis (dh/VEC per head); the FFN keeps
+//     whole VEC-channel chunks that hold at least one kept channel, with -1
+//     for the dropped channels inside them and for the padding to 64.
+//     No weights are copied.
+Layout build_layout(const dif_model* m, const dif_step_masks* mk, bool indexed) {
   const dif_config& c = m->cfg;
   const size_t es = esize(c.dtype);
+  const int vec = (int)(16 / es);
   const int D = c.dim, dh = c.head_dim, H = c.n_heads, F = c.ffn_dim;
   Layout L;
+  L.indexed = indexed;
   Carve cv;
   int jt, jh, jw;
   rope_pairs(dh, &jt, &jh, &jw);
   L.n_rope = (size_t)c.grid_f * jt + (size_t)c.grid_h * jh + (size_t)c.grid_w * jw;
   L.o_rope = cv.take(L.n_rope * 2 * sizeof(float));
   L.layers.resize(c.n_layers);
+  std::vector<int32_t>& ix = L.host_idx;
+  auto head_rows = [&](const uint8_t* keep) {
+    for (int i = 0; i < H; ++i)
+      if (keep[i])
+        for (int d = 0; d < dh; ++d) ix.push_back(i * dh + d);
+  };
+  auto head_chunks = [&](const uint8_t* keep) {
+    for (int i = 0; i < H; ++i)
+      if (keep[i])
+        for (int q = 0; q < dh / vec; ++q) ix.push_back((i * dh) / vec + q);
+  };
   for (int l = 0; l < c.n_layers; ++l) {
     LayerPlan& lp = L.layers[l];
     lp.info.block_keep = mk->block_keep[l];
-    int h = 0, hc = 0, f = 0;
+    const uint8_t* ks = mk->self_head_keep + (size_t)l * H;
+    const uint8_t* kc = mk->cross_head_keep + (size_t)l * H;
+    const uint8_t* kf = mk->ffn_keep + (size_t)l * F;
+    int h = 0, hc = 0, f = 0, touched = 0;
     for (int i = 0; i < H; ++i) {
-      h += mk->self_head_keep[(size_t)l * H + i];
-      hc += mk->cross_head_keep[(size_t)l * H + i];
+      h += ks[i];
+      hc += kc[i];
     }
-    for (int i = 0; i < F; ++i) f += mk->ffn_keep[(size_t)l * F + i];
+    for (int i = 0; i < F; ++i) f += kf[i];
+    for (int t = 0; indexed && t < F / vec; ++t) {
+      bool any = false;
+      for (int e = 0; e < vec; ++e) any = any || kf[t * vec + e];
+      touched += any;
+    }
     lp.info.self_heads = h;
     lp.info.cross_heads = hc;
     lp.info.ffn_channels = f;
-    lp.info.ffn_padded = (int)round_up(f, 64);
+    lp.info.ffn_padded = (int)round_up(indexed ? (int64_t)touched * vec : f, 64);
     if (!lp.info.block_keep) continue;
-    const int a = h * dh, ac = hc * dh, fp = lp.info.ffn_padded;
-    lp.h_idx_self = L.host_idx.size();
-    for (int i = 0; i < H; ++i)
-      if (mk->self_head_keep[(size_t)l * H + i])
-        for (int d = 0; d < dh; ++d) L.host_idx.push_back(i * dh + d);
-    lp.h_idx_cross = L.host_idx.size();
-    for (int i = 0; i < H; ++i)
-      if (mk->cross_head_keep[(size_t)l * H + i])
-        for (int d = 0; d < dh; ++d) L.host_idx.push_back(i * dh + d);
-    lp.h_idx_ffn = L.host_idx.size();
-    for (int i = 0; i < F; ++i)
-      if (mk->ffn_keep[(size_t)l * F + i]) L.host_idx.push_back(i);
-    for (int i = f; i < fp; ++i) L.host_idx.push_back(-1);
-    (void)a;
-    (void)ac;
+    const int fp = lp.info.ffn_padded;
+    lp.h_idx_self = ix.size();
+    head_rows(ks);
+    lp.h_idx_cross = ix.size();
+    head_rows(kc);
+    lp.h_idx_ffn = ix.size();
+    if (!indexed) {
+      for (int i = 0; i < F; ++i)
+        if (kf[i]) ix.push_back(i);
+    } else {
+      for (int t = 0; t < F / vec; ++t) {
+        bool any = false;
+        for (int e = 0; e < vec; ++e) any = any || kf[t * vec + e];
+        if (any)
+          for (int e = 0; e < vec; ++e) ix.push_back(kf[t * vec + e] ? t * vec + e : -1);
+      }
+    }
+    while ((int64_t)(ix.size() - lp.h_idx_ffn) < fp) ix.push_back(-1);
+    if (indexed) {
+      lp.h_kch_self = ix.size();
+      head_chunks(ks);
+      lp.h_kch_cross = ix.size();
+      head_chunks(kc);
+      lp.h_kch_ffn = ix.size();
+      for (int t = 0; t < F / vec; ++t) {
+        bool any = false;
+        for (int e = 0; e < vec; ++e) any = any || kf[t * vec + e];
+        if (any) ix.push_back(t);
+      }
+      while ((int64_t)(ix.size() - lp.h_kch_ffn) < fp / vec) ix.push_back(-1);
+    }
   }
-  L.o_idx = cv.take(L.host_idx.size() * sizeof(int32_t));
+  L.o_idx = cv.take(ix.size() * sizeof(int32_t));
   for (int l = 0; l < c.n_layers; ++l) {
     LayerPlan& lp = L.layers[l];
     if (!lp.info.block_keep) continue;
@@ -274,6 +337,12 @@ Layout build_layout(const dif_model* m, const dif_step_masks* mk) {
     lp.o_idx_self = L.o_idx + lp.h_idx_self * sizeof(int32_t);
     lp.o_idx_cross = L.o_idx + lp.h_idx_cross * sizeof(int32_t);
     lp.o_idx_ffn = L.o_idx + lp.h_idx_ffn * sizeof(int32_t);
+    if (indexed) {
+      lp.o_kch_self = L.o_idx + lp.h_kch_self * sizeof(int32_t);
+      lp.o_kch_cross = L.o_idx + lp.h_kch_cross * sizeof(int32_t);
+      lp.o_kch_ffn = L.o_idx + lp.h_kch_ffn * sizeof(int32_t);
+      continue;
+    }
     lp.o_wqkv = cv.take(3 * a * D * es);
     lp.o_bqkv = cv.take(3 * a * 4);
     lp.o_gq = cv.take(a * 4);
@@ -341,13 +410,13 @@ dif_status check_ws(const WsLayout& w, const void* ws, size_t bytes) {
 template <typename T, typename OutT>
 dif_status gemm(int kind, const T* A, int64_t lda, const T* Bm, int64_t ldb, OutT* C, int64_t ldc,
                 int M, int N, int K, int epi, const float* bias, const float* g0, const float* g1,
-                hipStream_t s) {
+                hipStream_t s, const dif::GemmGather* gather = nullptr) {
   if (M <= 0 || N <= 0) return DIF_OK;
   const double es = sizeof(T);
   const double bytes = ((double)M * K + (double)N * K) * es + (double)M * N * sizeof(OutT) *
                                                                    (epi == dif::EPI_RESIDUAL ? 2 : 1);
   ProfScope ps(kind, s, 2.0 * M * N * (double)K, bytes);
-  HIP_TRY((dif::launch_gemm<T, OutT>(A, lda, Bm, ldb, C, ldc, M, N, K, epi, bias, g0, g1, s)));
+  HIP_TRY((dif::launch_gemm<T, OutT>(A, lda, Bm, ldb, C, ldc, M, N, K, epi, bias, g0, g1, s, gather)));
   return DIF_OK;
 }
 
@@ -437,15 +506,36 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     ProfScope ps(PK_NORM, s, 0, 2.0 * M * D * es);
     HIP_TRY(dif::launch_norm<T>(x, xn, M, D, 0, mod, e0, mod + D, e0 + D, c.eps, s));
   }
+  // Compact plans read the step's gathered weights; indexed plans read the
+  // union weights through the tables (rows for output widths, 16-byte K
+  // chunks for reduction widths).
+  const bool ix = plan->lay.indexed;
+  const int32_t* rs = lp.at<int32_t>(lp.o_idx_self);
+  const int32_t* rc = lp.at<int32_t>(lp.o_idx_cross);
+  const int32_t* rf = lp.at<int32_t>(lp.o_idx_ffn);
+  const dif::GemmGather g_self_rows{rs, nullptr, D}, g_cross_rows{rc, nullptr, D},
+      g_ffn_rows{rf, nullptr, c.ffn_dim};
+  const dif::GemmGather g_self_k{nullptr, lp.at<int32_t>(lp.o_kch_self), 0},
+      g_cross_k{nullptr, lp.at<int32_t>(lp.o_kch_cross), 0},
+      g_ffn_k{nullptr, lp.at<int32_t>(lp.o_kch_ffn), 0};
   if (a > 0) {
-    DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, lp.at<T>(lp.o_wqkv), D, big, 3 * a, M, 3 * a, D,
-                        dif::EPI_STORE, lp.at<float>(lp.o_bqkv), nullptr, nullptr, s)));
+    if (ix) {
+      const void* wm[3] = {W.self_wq, W.self_wk, W.self_wv};
+      const float* bm[3] = {W.self_bq, W.self_bk, W.self_bv};
+      for (int q = 0; q < 3; ++q)
+        DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, (const T*)wm[q], D, big + (size_t)q * a, 3 * a, M, a,
+                            D, dif::EPI_STORE, bm[q], nullptr, nullptr, s, &g_self_rows)));
+    } else {
+      DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, lp.at<T>(lp.o_wqkv), D, big, 3 * a, M, 3 * a, D,
+                          dif::EPI_STORE, lp.at<float>(lp.o_bqkv), nullptr, nullptr, s)));
+    }
     {
       ProfScope ps(PK_QK_NORM, s, 0, 4.0 * M * a * es);
       dif::RopeDesc rd = plan->rope;
       rd.L = L;
-      HIP_TRY(dif::launch_qk_norm<T>(big, 3 * a, M, a, 2, 0, a, lp.at<float>(lp.o_gq),
-                                     lp.at<float>(lp.o_gk), inv_d, c.eps, &rd, s));
+      HIP_TRY(dif::launch_qk_norm<T>(big, 3 * a, M, a, 2, 0, a, ix ? W.self_gq : lp.at<float>(lp.o_gq),
+                                     ix ? W.self_gk : lp.at<float>(lp.o_gk), inv_d, c.eps, &rd, s,
+                                     ix ? rs : nullptr));
     }
     {
       ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * M * a * es);
@@ -454,8 +544,12 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     DIF_TRY(attention<T>(PK_ATTN_SELF, dh, big, 3 * a, big + a, 3 * a, vt, wl.ldvt, o, a, B, L, L,
                          lp.info.self_heads, s));
   }
-  DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), lp.at<T>(lp.o_wo), std::max(a, 8), x, D,
-                      M, D, a, dif::EPI_RESIDUAL, W.self_bo, mod + 2 * D, e0 + 2 * D, s)));
+  if (ix)
+    DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), (const T*)W.self_wo, D, x, D, M, D, a,
+                        dif::EPI_RESIDUAL, W.self_bo, mod + 2 * D, e0 + 2 * D, s, &g_self_k)));
+  else
+    DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), lp.at<T>(lp.o_wo), std::max(a, 8), x, D,
+                        M, D, a, dif::EPI_RESIDUAL, W.self_bo, mod + 2 * D, e0 + 2 * D, s)));
 
   // cross-attention to the text tokens
   {
@@ -464,16 +558,26 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
   }
   if (ac > 0) {
     T* cq = big;
-    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, lp.at<T>(lp.o_wcq), D, cq, ac, M, ac, D,
-                        dif::EPI_STORE, lp.at<float>(lp.o_bcq), nullptr, nullptr, s)));
-    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, lp.at<T>(lp.o_wckv), D, ckv, 2 * ac, Mc, 2 * ac, D,
-                        dif::EPI_STORE, lp.at<float>(lp.o_bckv), nullptr, nullptr, s)));
+    if (ix) {
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, (const T*)W.cross_wq, D, cq, ac, M, ac, D,
+                          dif::EPI_STORE, W.cross_bq, nullptr, nullptr, s, &g_cross_rows)));
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wk, D, ckv, 2 * ac, Mc, ac, D,
+                          dif::EPI_STORE, W.cross_bk, nullptr, nullptr, s, &g_cross_rows)));
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wv, D, ckv + ac, 2 * ac, Mc, ac,
+                          D, dif::EPI_STORE, W.cross_bv, nullptr, nullptr, s, &g_cross_rows)));
+    } else {
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, lp.at<T>(lp.o_wcq), D, cq, ac, M, ac, D,
+                          dif::EPI_STORE, lp.at<float>(lp.o_bcq), nullptr, nullptr, s)));
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, lp.at<T>(lp.o_wckv), D, ckv, 2 * ac, Mc, 2 * ac, D,
+                          dif::EPI_STORE, lp.at<float>(lp.o_bckv), nullptr, nullptr, s)));
+    }
     {
       ProfScope ps(PK_QK_NORM, s, 0, 2.0 * (M + Mc) * ac * es);
-      HIP_TRY(dif::launch_qk_norm<T>(cq, ac, M, ac, 1, 0, 0, lp.at<float>(lp.o_gcq), nullptr, inv_d,
-                                     c.eps, nullptr, s));
-      HIP_TRY(dif::launch_qk_norm<T>(ckv, 2 * ac, Mc, ac, 1, 0, 0, lp.at<float>(lp.o_gck), nullptr,
-                                     inv_d, c.eps, nullptr, s));
+      HIP_TRY(dif::launch_qk_norm<T>(cq, ac, M, ac, 1, 0, 0, ix ? W.cross_gq : lp.at<float>(lp.o_gcq),
+                                     nullptr, inv_d, c.eps, nullptr, s, ix ? rc : nullptr));
+      HIP_TRY(dif::launch_qk_norm<T>(ckv, 2 * ac, Mc, ac, 1, 0, 0,
+                                     ix ? W.cross_gk : lp.at<float>(lp.o_gck), nullptr, inv_d, c.eps,
+                                     nullptr, s, ix ? rc : nullptr));
     }
     {
       ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * Mc * ac * es);
@@ -482,8 +586,12 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     DIF_TRY(attention<T>(PK_ATTN_CROSS, dh, cq, ac, ckv, 2 * ac, cvt, wl.ldcvt, o, ac, B, L, Lc,
                          lp.info.cross_heads, s));
   }
-  DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_OUT, o, std::max(ac, 8), lp.at<T>(lp.o_wco), std::max(ac, 8), x, D,
-                      M, D, ac, dif::EPI_RESIDUAL, W.cross_bo, nullptr, nullptr, s)));
+  if (ix)
+    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_OUT, o, std::max(ac, 8), (const T*)W.cross_wo, D, x, D, M, D, ac,
+                        dif::EPI_RESIDUAL, W.cross_bo, nullptr, nullptr, s, &g_cross_k)));
+  else
+    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_OUT, o, std::max(ac, 8), lp.at<T>(lp.o_wco), std::max(ac, 8), x,
+                        D, M, D, ac, dif::EPI_RESIDUAL, W.cross_bo, nullptr, nullptr, s)));
 
   // FFN: LN + AdaLN(shift2, scale2), GELU, gate2
   {
@@ -491,11 +599,19 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     HIP_TRY(dif::launch_norm<T>(x, xn, M, D, 0, mod + 3 * D, e0 + 3 * D, mod + 4 * D, e0 + 4 * D,
                                 c.eps, s));
   }
-  if (fp > 0)
-    DIF_TRY((gemm<T, T>(PK_GEMM_FFN1, xn, D, lp.at<T>(lp.o_w1), D, big, fp, M, fp, D, dif::EPI_GELU,
-                        lp.at<float>(lp.o_b1), nullptr, nullptr, s)));
-  DIF_TRY((gemm<T, T>(PK_GEMM_FFN2, big, std::max(fp, 8), lp.at<T>(lp.o_w2), std::max(fp, 8), x, D,
-                      M, D, fp, dif::EPI_RESIDUAL, W.ffn_b2, mod + 5 * D, e0 + 5 * D, s)));
+  if (ix) {
+    if (fp > 0)
+      DIF_TRY((gemm<T, T>(PK_GEMM_FFN1, xn, D, (const T*)W.ffn_w1, D, big, fp, M, fp, D, dif::EPI_GELU,
+                          W.ffn_b1, nullptr, nullptr, s, &g_ffn_rows)));
+    DIF_TRY((gemm<T, T>(PK_GEMM_FFN2, big, std::max(fp, 8), (const T*)W.ffn_w2, c.ffn_dim, x, D, M, D,
+                        fp, dif::EPI_RESIDUAL, W.ffn_b2, mod + 5 * D, e0 + 5 * D, s, &g_ffn_k)));
+  } else {
+    if (fp > 0)
+      DIF_TRY((gemm<T, T>(PK_GEMM_FFN1, xn, D, lp.at<T>(lp.o_w1), D, big, fp, M, fp, D, dif::EPI_GELU,
+                          lp.at<float>(lp.o_b1), nullptr, nullptr, s)));
+    DIF_TRY((gemm<T, T>(PK_GEMM_FFN2, big, std::max(fp, 8), lp.at<T>(lp.o_w2), std::max(fp, 8), x, D,
+                        M, D, fp, dif::EPI_RESIDUAL, W.ffn_b2, mod + 5 * D, e0 + 5 * D, s)));
+  }
   return DIF_OK;
 }
 
@@ -628,23 +744,36 @@ dif_status dif_model_destroy(dif_model* model) {
   return DIF_OK;
 }
 
-dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, size_t* bytes) {
+dif_status dif_plan_bytes_ex(const dif_model* model, const dif_step_masks* masks, int32_t kind,
+                            size_t* bytes) {
   GUARD_BEGIN
   if (!model || !bytes) return fail(DIF_E_ARG, "null argument");
+  DIF_TRY(check_plan_kind(&model->cfg, kind));
   DIF_TRY(check_masks(&model->cfg, masks));
-  *bytes = build_layout(model, masks).total;
+  *bytes = build_layout(model, masks, kind == DIF_PLAN_INDEXED).total;
   return DIF_OK;
   GUARD_END
 }
 
+dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, size_t* bytes) {
+  return dif_plan_bytes_ex(model, masks, DIF_PLAN_COMPACT, bytes);
+}
+
 dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_masks* masks,
                          void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out) {
+  return dif_plan_step_ex(model, step, masks, DIF_PLAN_COMPACT, plan_mem, plan_bytes, stream, out);
+}
+
+dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step_masks* masks,
+                            int32_t kind, void* plan_mem, size_t plan_bytes, dif_stream stream,
+                            dif_plan** out) {
   GUARD_BEGIN
   if (!model || !out) return fail(DIF_E_ARG, "null argument");
   *out = nullptr;
   if (step < 0 || step >= 4096) return fail(DIF_E_ARG, "step %d out of range", step);
+  DIF_TRY(check_plan_kind(&model->cfg, kind));
   DIF_TRY(check_masks(&model->cfg, masks));
-  Layout lay = build_layout(model, masks);
+  Layout lay = build_layout(model, masks, kind == DIF_PLAN_INDEXED);
   if (!plan_mem) return fail(DIF_E_WORKSPACE, "plan memory is null");
   if (reinterpret_cast<uintptr_t>(plan_mem) % 256) return fail(DIF_E_WORKSPACE, "plan memory not 256-byte aligned");
   if (plan_bytes < lay.total)
@@ -685,7 +814,7 @@ dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_ma
       hipMemcpyAsync(p->mem + p->lay.o_idx, p->lay.host_idx.data(),
                      p->lay.host_idx.size() * sizeof(int32_t), hipMemcpyHostToDevice, s) != hipSuccess)
     return cleanup(fail(DIF_E_HIP, "index table upload failed"));
-  for (int l = 0; l < c.n_layers; ++l) {
+  for (int l = 0; l < c.n_layers && !p->lay.indexed; ++l) {
     const LayerPlan& lp = p->lay.layers[l];
     if (!lp.info.block_keep) continue;
     const dif_status st = c.dtype == DIF_BF16 ? gather_layer<bf16>(model, l, lp, s)

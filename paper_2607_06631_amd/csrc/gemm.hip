@@ -12,12 +12,27 @@
 // staging sets.  Ragged M and N: rows past the matrix read as zero through
 // the descriptor bounds and stores are predicated; K must be a multiple of
 // the k-tile (the plan pads pruned widths to 64).
+//
+// Index-table gather (the step's active parameters read in place from the
+// union weight set, no compacted copy):
+//   GA_ROWS  output column n uses B row rows[n] (-1: a zero row); the bias
+//            is gathered the same way.  Used where whole heads or FFN
+//            channels are dropped from the output width.
+//   GA_KCH   16-byte K chunk c of every B row is read from chunk kch[c] of
+//            that row (-1: zeros).  Used where dropped heads or FFN chunks
+//            shorten the reduction.  The chunk table is staged in LDS once.
+// Masked rows / chunks get an offset past the descriptor's range, which the
+// buffer load returns as zero.
 #include "common.h"
 #include "kernels.h"
 
 namespace dif {
 
-constexpr int G_CH = 8;  // 16-byte chunks per k-tile row (128 bytes)
+constexpr int G_CH = 8;     // 16-byte chunks per k-tile row (128 bytes)
+constexpr int BN_MAX = 256; // largest workgroup tile width over the shapes below
+
+enum { GA_NONE = 0, GA_ROWS = 1, GA_KCH = 2 };
+constexpr uint32_t kMasked = 0x80000000u;  // buffer offset beyond any descriptor range
 
 template <typename T, typename OutT>
 struct GemmParams {
@@ -29,10 +44,13 @@ struct GemmParams {
   const float* bias;
   const float* gate0;
   const float* gate1;
+  const int32_t* rows;   // GA_ROWS
+  const int32_t* kch;    // GA_KCH
+  int b_rows;            // GA_ROWS: rows of the union B matrix
 };
 
 // WGM x WGN waves; each wave owns TM x TN MFMA 32x32 tiles.
-template <typename T, typename OutT, int EPI, int WGM, int WGN, int TM, int TN>
+template <typename T, typename OutT, int EPI, int GA, int WGM, int WGN, int TM, int TN>
 __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, OutT> p) {
   constexpr int NT = 64 * WGM * WGN;
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
@@ -42,6 +60,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   constexpr int LA = BM / RPL, LB = BN / RPL;
   static_assert(LA * RPL == BM && LB * RPL == BN, "staging split");
   __shared__ u32x4 smem[2][BM + BN][G_CH];
+  extern __shared__ uint32_t kch_lds[];   // GA_KCH: byte offset of each K chunk
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
@@ -65,19 +84,39 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   const int lc = tid & 7, lr = tid >> 3;
   constexpr uint32_t kRsrcWord3 = 0x00020000u;
   const uint32_t a_bytes = (uint32_t)(min(BM, p.M - m0) * p.lda * (int64_t)sizeof(T));
-  const uint32_t b_bytes = (uint32_t)(min(BN, p.N - n0) * p.ldb * (int64_t)sizeof(T));
+  // GA_ROWS: one descriptor over the whole union matrix, rows picked per thread
+  const uint32_t b_bytes =
+      GA == GA_ROWS ? (uint32_t)((int64_t)p.b_rows * p.ldb * (int64_t)sizeof(T))
+                    : (uint32_t)(min(BN, p.N - n0) * p.ldb * (int64_t)sizeof(T));
+  const T* b_base = GA == GA_ROWS ? p.B : p.B + (int64_t)n0 * p.ldb;
   const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<T*>(p.A + (int64_t)m0 * p.lda), (short)0, a_bytes, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t b_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<T*>(p.B + (int64_t)n0 * p.ldb), (short)0, b_bytes, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t b_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(b_base), (short)0, b_bytes, kRsrcWord3);
   uint32_t a_off[LA], b_off[LB];
 #pragma unroll
   for (int i = 0; i < LA; ++i)
     a_off[i] = (uint32_t)(((lr + RPL * i) * p.lda + lc * VEC) * (int64_t)sizeof(T));
 #pragma unroll
-  for (int i = 0; i < LB; ++i)
-    b_off[i] = (uint32_t)(((lr + RPL * i) * p.ldb + lc * VEC) * (int64_t)sizeof(T));
+  for (int i = 0; i < LB; ++i) {
+    if constexpr (GA == GA_ROWS) {
+      const int n = n0 + lr + RPL * i;
+      const int r = n < p.N ? p.rows[n] : -1;
+      b_off[i] = r >= 0 ? (uint32_t)((r * p.ldb + lc * VEC) * (int64_t)sizeof(T)) : kMasked;
+    } else if constexpr (GA == GA_KCH) {
+      b_off[i] = (uint32_t)((lr + RPL * i) * p.ldb * (int64_t)sizeof(T));   // chunk added per k-tile
+    } else {
+      b_off[i] = (uint32_t)(((lr + RPL * i) * p.ldb + lc * VEC) * (int64_t)sizeof(T));
+    }
+  }
   const int nk = p.K / BK;
+  if constexpr (GA == GA_KCH) {
+    for (int c = tid; c < p.K / VEC; c += NT) {
+      const int u = p.kch[c];
+      kch_lds[c] = u >= 0 ? (uint32_t)u * 16u : kMasked;
+    }
+    __syncthreads();
+  }
 
   // Two register staging sets: tile kt+2 is requested while tile kt is
   // computed, so global latency is hidden behind two compute phases.
@@ -87,9 +126,16 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
 #pragma unroll
     for (int i = 0; i < LA; ++i)
       ra[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_off[i], koff, 0));
+    if constexpr (GA == GA_KCH) {
+      const uint32_t kb = kch_lds[kt * G_CH + lc];
 #pragma unroll
-    for (int i = 0; i < LB; ++i)
-      rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i], koff, 0));
+      for (int i = 0; i < LB; ++i)
+        rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i] + kb, 0, 0));
+    } else {
+#pragma unroll
+      for (int i = 0; i < LB; ++i)
+        rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i], koff, 0));
+    }
   };
   auto sstore = [&](int buf, const u32x4* ra, const u32x4* rb) {
 #pragma unroll
@@ -154,7 +200,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   for (int j = 0; j < TN; ++j) {
     const int n = n0 + wn * TN * 32 + j * 32 + col;
     if (n >= p.N) continue;
-    const float bias = p.bias ? p.bias[n] : 0.f;
+    float bias = 0.f;
+    if constexpr (GA == GA_ROWS) {
+      const int r = p.rows[n];
+      if (p.bias && r >= 0) bias = p.bias[r];
+    } else {
+      if (p.bias) bias = p.bias[n];
+    }
     float gate = 1.f;
     if (EPI == EPI_RESIDUAL && p.gate0) gate = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
 #pragma unroll
@@ -184,7 +236,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
 #define DIF_GEMM_WAVES 8
 #endif
 
-template <typename T, typename OutT, int EPI>
+// LDS left beside the two 64 KB operand buffers for the K-chunk table
+constexpr int kMaxKChunks = (160 * 1024 - 2 * 64 * 1024) / 4;
+
+template <typename T, typename OutT, int EPI, int GA>
 void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
 #if DIF_GEMM_WAVES == 4
   constexpr int WGM = 2, WGN = 2, TM = 4, TN = 4;
@@ -193,32 +248,53 @@ void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
 #endif
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
-  hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI, WGM, WGN, TM, TN>), dim3(tiles),
-                     dim3(64 * WGM * WGN), 0, stream, p);
+  const size_t dyn = GA == GA_KCH ? (size_t)(p.K / Chunk<T>::VEC) * sizeof(uint32_t) : 0;
+  hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI, GA, WGM, WGN, TM, TN>), dim3(tiles),
+                     dim3(64 * WGM * WGN), dyn, stream, p);
 }
 
 template <typename T, typename OutT>
 hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
-                       const float* gate1, hipStream_t stream) {
+                       const float* gate1, hipStream_t stream, const GemmGather* gather) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  GemmParams<T, OutT> p{A, B, C, lda, ldb, ldc, M, N, K, bias, gate0, gate1};
-  switch (epi) {
-    case EPI_STORE: launch_tile<T, OutT, EPI_STORE>(p, stream); break;
-    case EPI_GELU: launch_tile<T, OutT, EPI_GELU>(p, stream); break;
-    default: launch_tile<T, OutT, EPI_RESIDUAL>(p, stream); break;
+  GemmParams<T, OutT> p{A, B, C, lda, ldb, ldc, M, N, K, bias, gate0, gate1, nullptr, nullptr, 0};
+  if (!gather || (!gather->rows && !gather->kchunks)) {
+    switch (epi) {
+      case EPI_STORE: launch_tile<T, OutT, EPI_STORE, GA_NONE>(p, stream); break;
+      case EPI_GELU: launch_tile<T, OutT, EPI_GELU, GA_NONE>(p, stream); break;
+      default: launch_tile<T, OutT, EPI_RESIDUAL, GA_NONE>(p, stream); break;
+    }
+  } else if (gather->rows && !gather->kchunks) {
+    // the whole union matrix must stay addressable below the masked offset
+    if (gather->b_rows <= 0 || (int64_t)gather->b_rows * ldb * (int64_t)sizeof(T) >= (int64_t)kMasked)
+      return hipErrorInvalidValue;
+    p.rows = gather->rows;
+    p.b_rows = gather->b_rows;
+    switch (epi) {
+      case EPI_STORE: launch_tile<T, OutT, EPI_STORE, GA_ROWS>(p, stream); break;
+      case EPI_GELU: launch_tile<T, OutT, EPI_GELU, GA_ROWS>(p, stream); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else if (gather->kchunks && !gather->rows) {
+    if (epi != EPI_RESIDUAL || K / Chunk<T>::VEC > kMaxKChunks ||
+        (int64_t)BN_MAX * ldb * (int64_t)sizeof(T) >= (int64_t)kMasked)
+      return hipErrorInvalidValue;
+    p.kch = gather->kchunks;
+    launch_tile<T, OutT, EPI_RESIDUAL, GA_KCH>(p, stream);
+  } else {
+    return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template hipError_t launch_gemm<bf16, bf16>(const bf16*, int64_t, const bf16*, int64_t, bf16*, int64_t,
-                                            int, int, int, int, const float*, const float*,
-                                            const float*, hipStream_t);
-template hipError_t launch_gemm<bf16, float>(const bf16*, int64_t, const bf16*, int64_t, float*, int64_t,
-                                             int, int, int, int, const float*, const float*,
-                                             const float*, hipStream_t);
-template hipError_t launch_gemm<float, float>(const float*, int64_t, const float*, int64_t, float*,
-                                              int64_t, int, int, int, int, const float*,
-                                              const float*, const float*, hipStream_t);
+#define INST(T, OutT)                                                                         \
+  template hipError_t launch_gemm<T, OutT>(const T*, int64_t, const T*, int64_t, OutT*, int64_t, \
+                                           int, int, int, int, const float*, const float*,    \
+                                           const float*, hipStream_t, const GemmGather*);
+INST(bf16, bf16)
+INST(bf16, float)
+INST(float, float)
+#undef INST
 
 }  // namespace dif

@@ -10,11 +10,23 @@ typedef __bf16 bf16;
 
 enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESIDUAL = 2 };
 
+// Optional index-table gather of the B operand from a union weight matrix.
+//   rows:    B row of each of the N output columns (-1: zero row, zero bias);
+//            b_rows = rows of the union matrix.  Epilogues STORE and GELU.
+//   kchunks: for each 16-byte chunk c of the K extent, the chunk of every B
+//            row it is read from (-1: zeros); at most 8192 chunks.  Epilogue
+//            RESIDUAL.  A operand columns are compacted as K.
+struct GemmGather {
+  const int32_t* rows;
+  const int32_t* kchunks;
+  int b_rows;
+};
+
 // C[M,N] = epi(A[M,K] * B[N,K]^T); T in {float, __bf16}; OutT in {T, float}.
 template <typename T, typename OutT>
 hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
-                       const float* gate1, hipStream_t stream);
+                       const float* gate1, hipStream_t stream, const GemmGather* gather = nullptr);
 
 // Flash attention; V given transposed (see dif_attention in dif.h).
 template <typename T>
@@ -31,7 +43,8 @@ hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0
                        hipStream_t stream);
 
 // In place on rows of buf (stride ld): for each of nseg segments of width a
-// at column offset off[s]: y = x / sqrt(sum(x^2) * inv_norm_dim + eps) * gain[s][c],
+// at column offset off[s]: y = x / sqrt(sum(x^2) * inv_norm_dim + eps) * gain[s][idx[c]]
+// (idx null: identity),
 // then (rope != null) rotate consecutive pairs of each head_dim-wide head by
 // the token's 3D angles.
 struct RopeDesc {
@@ -44,7 +57,8 @@ struct RopeDesc {
 template <typename T>
 hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off0, int off1,
                           const float* g0, const float* g1, float inv_norm_dim, float eps,
-                          const RopeDesc* rope, hipStream_t stream);
+                          const RopeDesc* rope, hipStream_t stream,
+                          const int32_t* gain_idx = nullptr);
 
 // Vt[(b*a + c)*ldvt + j] = src[(b*Lk + j)*lds + c] for j < Lk, 0 for Lk <= j < ldvt.
 template <typename T>

@@ -27,13 +27,13 @@ def _rows(L, seed, n=160):
                                      np.arange(L - 40, L)]))
 
 
-def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False):
+def _run(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="compact"):
     import torch
     one = cfg.with_(n_layers=1)
     m1 = {k: v[layer:layer + 1] for k, v in masks.items()}
     say(f"{cfg.name}: L={cfg.seq_len} layer={layer} heads={int(m1['self_head_keep'].sum())} "
         f"cross={int(m1['cross_head_keep'].sum())} ffn={int(m1['ffn_keep'].sum())} "
-        f"{'ffn-gate-off ' if gate_ffn_off else ''}seed={seed}")
+        f"{'ffn-gate-off ' if gate_ffn_off else ''}seed={seed} plan={kind}")
     x = synth.make_block_input(one, seed, scale=x_scale)
     ctx = synth.make_context(one, seed)
     e0 = synth.make_e0(one, seed, std=0.3)
@@ -42,14 +42,19 @@ def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False):
     w = synth.make_global_weights(one, 0)
     w["layers"] = [wl]
     model = make_model(one, w)
-    plan = B.dif_plan_step(model, 0, m1)
+    plan = B.dif_plan_step(model, 0, m1, kind=kind)
     xd, cd = to_dev(x, one), to_dev(ctx, one)
     ed = to_dev(e0, dtype=torch.float32)
     ws = B.workspace(model, 1, one.seq_len, one.text_len)
     B.dif_block_forward(plan, 0, xd, cd, ed, ws)
     torch.cuda.synchronize()
     got = to_np(xd)[0]
-    say("  GPU block done; oracle on sampled rows")
+    return one, m1, x, ctx, e0, got
+
+
+def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="compact"):
+    one, m1, x, ctx, e0, got = _run(cfg, wl, masks, layer, seed, x_scale, gate_ffn_off, kind)
+    say(f"  GPU block done ({kind} plan); oracle on sampled rows")
     rows = _rows(one.seq_len, seed)
     wz = O.apply_keep(wl, m1["self_head_keep"][0], m1["cross_head_keep"][0], m1["ffn_keep"][0],
                       one.head_dim, np.float32)
@@ -95,3 +100,22 @@ def test_wan14b_720p_block_fullsize():
     masks = synth.make_masks(cfg, 1)
     wl = synth.make_layer_weights(cfg, 0, 0)
     _check(cfg, wl, masks, 0, seed=60, gate_ffn_off=True)
+
+
+def test_wan14b_block_fullsize_indexed_per_channel(c3_layer):
+    """Indexed plan (weights read in place through I_t) with the 14B block's
+    per-channel FFN count at t3 (9677 channels)."""
+    cfg, wl = c3_layer
+    _check(cfg, wl, synth.make_masks(cfg, 2), 0, seed=70, gate_ffn_off=False, kind="indexed")
+
+
+def test_wan14b_480p_indexed_equals_compact():
+    """The benchmark's structures use C = 8 chunks: both plan kinds give the
+    same bits on a full-size layer."""
+    cfg = get_config("wan14b_480p")
+    masks = synth.make_masks(cfg, 1)
+    layer = 7
+    wl = synth.make_layer_weights(cfg, layer, 0)
+    got_i = _run(cfg, wl, masks, layer, seed=71, kind="indexed")[-1]
+    got_c = _run(cfg, wl, masks, layer, seed=71, kind="compact")[-1]
+    assert np.array_equal(got_i, got_c)
