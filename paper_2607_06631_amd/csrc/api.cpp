@@ -413,9 +413,10 @@ dif_status gemm(int kind, const T* A, int64_t lda, const T* Bm, int64_t ldb, Out
                 hipStream_t s, const dif::GemmGather* gather = nullptr) {
   if (M <= 0 || N <= 0) return DIF_OK;
   const double es = sizeof(T);
-  const double bytes = ((double)M * K + (double)N * K) * es + (double)M * N * sizeof(OutT) *
-                                                                   (epi == dif::EPI_RESIDUAL ? 2 : 1);
-  ProfScope ps(kind, s, 2.0 * M * N * (double)K, bytes);
+  const double Nt = (double)N * (gather ? gather->nseg : 1);   // all segments
+  const double bytes = ((double)M * K + Nt * K) * es + (double)M * Nt * sizeof(OutT) *
+                                                          (epi == dif::EPI_RESIDUAL ? 2 : 1);
+  ProfScope ps(kind, s, 2.0 * M * Nt * (double)K, bytes);
   HIP_TRY((dif::launch_gemm<T, OutT>(A, lda, Bm, ldb, C, ldc, M, N, K, epi, bias, g0, g1, s, gather)));
   return DIF_OK;
 }
@@ -423,12 +424,12 @@ dif_status gemm(int kind, const T* A, int64_t lda, const T* Bm, int64_t ldb, Out
 template <typename T>
 dif_status attention(int kind, int dh, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                      const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk, int H,
-                     hipStream_t s) {
+                     hipStream_t s, bool q_scaled = false) {
   if (H <= 0) return DIF_OK;
   const double flops = 4.0 * B * (double)Lq * Lk * dh * H;
   const double bytes = (double)B * (2.0 * Lq + 2.0 * Lk) * H * dh * sizeof(T);
   ProfScope ps(kind, s, flops, bytes);
-  HIP_TRY(dif::launch_attention<T>(dh, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk, H, s));
+  HIP_TRY(dif::launch_attention<T>(dh, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk, H, s, q_scaled));
   return DIF_OK;
 }
 
@@ -493,6 +494,8 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
   const int a = lp.info.self_heads * dh, ac = lp.info.cross_heads * dh, fp = lp.info.ffn_padded;
   const float* mod = W.mod;
   const float inv_d = 1.f / (float)D;
+  // queries leave QK-norm already multiplied by the softmax scale in base 2
+  const float q_scale = (float)(1.4426950408889634 / std::sqrt((double)dh));
   T* xn = reinterpret_cast<T*>(ws + wl.xn);
   T* big = reinterpret_cast<T*>(ws + wl.big);
   T* vt = reinterpret_cast<T*>(ws + wl.vt);
@@ -520,11 +523,14 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       g_ffn_k{nullptr, lp.at<int32_t>(lp.o_kch_ffn), 0};
   if (a > 0) {
     if (ix) {
-      const void* wm[3] = {W.self_wq, W.self_wk, W.self_wv};
-      const float* bm[3] = {W.self_bq, W.self_bk, W.self_bv};
-      for (int q = 0; q < 3; ++q)
-        DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, (const T*)wm[q], D, big + (size_t)q * a, 3 * a, M, a,
-                            D, dif::EPI_STORE, bm[q], nullptr, nullptr, s, &g_self_rows)));
+      dif::GemmGather g = g_self_rows;
+      g.nseg = 3;
+      g.seg_b[0] = W.self_wk;
+      g.seg_b[1] = W.self_wv;
+      g.seg_bias[0] = W.self_bk;
+      g.seg_bias[1] = W.self_bv;
+      DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, (const T*)W.self_wq, D, big, 3 * a, M, a, D,
+                          dif::EPI_STORE, W.self_bq, nullptr, nullptr, s, &g)));
     } else {
       DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, lp.at<T>(lp.o_wqkv), D, big, 3 * a, M, 3 * a, D,
                           dif::EPI_STORE, lp.at<float>(lp.o_bqkv), nullptr, nullptr, s)));
@@ -535,14 +541,14 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       rd.L = L;
       HIP_TRY(dif::launch_qk_norm<T>(big, 3 * a, M, a, 2, 0, a, ix ? W.self_gq : lp.at<float>(lp.o_gq),
                                      ix ? W.self_gk : lp.at<float>(lp.o_gk), inv_d, c.eps, &rd, s,
-                                     ix ? rs : nullptr));
+                                     ix ? rs : nullptr, q_scale));
     }
     {
       ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * M * a * es);
       HIP_TRY(dif::launch_transpose_vt<T>(big + 2 * a, 3 * a, a, B, L, vt, wl.ldvt, s));
     }
     DIF_TRY(attention<T>(PK_ATTN_SELF, dh, big, 3 * a, big + a, 3 * a, vt, wl.ldvt, o, a, B, L, L,
-                         lp.info.self_heads, s));
+                         lp.info.self_heads, s, true));
   }
   if (ix)
     DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), (const T*)W.self_wo, D, x, D, M, D, a,
@@ -561,10 +567,12 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     if (ix) {
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, (const T*)W.cross_wq, D, cq, ac, M, ac, D,
                           dif::EPI_STORE, W.cross_bq, nullptr, nullptr, s, &g_cross_rows)));
+      dif::GemmGather g = g_cross_rows;
+      g.nseg = 2;
+      g.seg_b[0] = W.cross_wv;
+      g.seg_bias[0] = W.cross_bv;
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wk, D, ckv, 2 * ac, Mc, ac, D,
-                          dif::EPI_STORE, W.cross_bk, nullptr, nullptr, s, &g_cross_rows)));
-      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wv, D, ckv + ac, 2 * ac, Mc, ac,
-                          D, dif::EPI_STORE, W.cross_bv, nullptr, nullptr, s, &g_cross_rows)));
+                          dif::EPI_STORE, W.cross_bk, nullptr, nullptr, s, &g)));
     } else {
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, lp.at<T>(lp.o_wcq), D, cq, ac, M, ac, D,
                           dif::EPI_STORE, lp.at<float>(lp.o_bcq), nullptr, nullptr, s)));
@@ -574,7 +582,7 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
     {
       ProfScope ps(PK_QK_NORM, s, 0, 2.0 * (M + Mc) * ac * es);
       HIP_TRY(dif::launch_qk_norm<T>(cq, ac, M, ac, 1, 0, 0, ix ? W.cross_gq : lp.at<float>(lp.o_gcq),
-                                     nullptr, inv_d, c.eps, nullptr, s, ix ? rc : nullptr));
+                                     nullptr, inv_d, c.eps, nullptr, s, ix ? rc : nullptr, q_scale));
       HIP_TRY(dif::launch_qk_norm<T>(ckv, 2 * ac, Mc, ac, 1, 0, 0,
                                      ix ? W.cross_gk : lp.at<float>(lp.o_gck), nullptr, inv_d, c.eps,
                                      nullptr, s, ix ? rc : nullptr));
@@ -584,7 +592,7 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       HIP_TRY(dif::launch_transpose_vt<T>(ckv + ac, 2 * ac, ac, B, Lc, cvt, wl.ldcvt, s));
     }
     DIF_TRY(attention<T>(PK_ATTN_CROSS, dh, cq, ac, ckv, 2 * ac, cvt, wl.ldcvt, o, ac, B, L, Lc,
-                         lp.info.cross_heads, s));
+                         lp.info.cross_heads, s, true));
   }
   if (ix)
     DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_OUT, o, std::max(ac, 8), (const T*)W.cross_wo, D, x, D, M, D, ac,

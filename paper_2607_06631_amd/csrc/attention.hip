@@ -1,10 +1,7 @@
 // Bidirectional flash attention on MFMA for gfx950.
 //
-// Work split: one workgroup = 4 waves of one (sample, head); a wave owns
-// QG groups of 32 queries and walks all keys in tiles of 64.  Each K and
-// V^T fragment read from LDS feeds the QG query groups, which halves LDS
-// read traffic per MFMA at QG = 2 (the LDS port, not the MFMA pipe, bounds
-// the one-group variant).
+// Work split: one workgroup = 4 waves of one (sample, head); a wave owns 32
+// queries and walks all keys in tiles of 64, as two 32-key halves.
 //
 // The scores are computed transposed, S^T = K Q^T, with MFMA 32x32 tiles:
 // the A operand is the K tile (rows = keys, from LDS), the B operand is
@@ -17,21 +14,24 @@
 // matching V^T operand one contiguous 16-byte LDS read.  V is consumed
 // transposed (Vt, [head_dim rows][keys]) so that read is row-contiguous.
 //
-// Online softmax in base 2 (scores pre-multiplied by log2(e)/sqrt(dh))
-// with a lazy rescale: the exponent base only moves (and O^T, l are
-// rescaled) when a query's running max exceeds it by more than kSlack.
+// Online softmax in base 2 with a lazy rescale: the exponent base m only
+// moves (and O^T, l are rescaled) when a query's scores exceed it by more
+// than kSlack.  The base enters through the MFMA accumulator: the first
+// MFMA of a half adds C = -m (sixteen registers that change only with m), so
+// with queries pre-scaled by log2(e)/sqrt(dh) (done by the QK-norm kernel
+// before its bf16 rounding) the MFMA output is already the exponent and the
+// VALU does no per-score scale or subtraction.  Unscaled queries (the plain
+// operator) take one multiply per score instead.
 // Key tails are masked to -inf; V^T chunks past the last key are zero-filled.
-// At QG = 1 the kernel fits in 256 registers per lane (two waves per SIMD);
-// at QG = 2 it runs one wave per SIMD with the accumulators in AGPRs.
+// The kernel fits in 256 registers per lane (two waves per SIMD).
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
 namespace dif {
 
-#ifndef DIF_ATTN_WAVES
-#define DIF_ATTN_WAVES 4
-#endif
-constexpr int AT_WAVES = DIF_ATTN_WAVES;
+constexpr int AT_WAVES = 4;
 constexpr int AT_THREADS = 64 * AT_WAVES;
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
@@ -53,10 +53,9 @@ __device__ __forceinline__ int key_slot(int kappa) {
   return 8 * k + 4 * gq + j;
 }
 
-// QG groups of 32 queries per wave: every K / V^T fragment read from LDS
-// feeds QG MFMAs.
-template <typename T, int DH, int QG>
-__global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_attn_kernel(AttnParams<T> p) {
+// SC: queries arrive pre-multiplied by log2(e)/sqrt(dh).
+template <typename T, int DH, bool SC>
+__global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(AttnParams<T> p) {
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int KCH = DH * (int)sizeof(T) / 16;     // chunks per K row
   constexpr int VCH = AT_BN * (int)sizeof(T) / 16;  // chunks per V^T row
@@ -64,7 +63,7 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_
   constexpr int NPC = 16 / VEC;                     // P chunks per 32-key sub-tile
   constexpr int K_PER_T = AT_BN * KCH / AT_THREADS;
   constexpr int V_PER_T = DH * VCH / AT_THREADS;
-  constexpr int BMQ = AT_WAVES * 32 * QG;           // queries per workgroup
+  constexpr int BMQ = AT_WAVES * 32;                // queries per workgroup
   static_assert(K_PER_T * AT_THREADS == AT_BN * KCH, "K tile split");
   static_assert(V_PER_T * AT_THREADS == DH * VCH, "V tile split");
   __shared__ u32x4 ks_[2][AT_BN][KCH];
@@ -78,15 +77,14 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_
   const int qb = bid % nqb, hb = bid / nqb;
   const int h = hb % p.H, b = hb / p.H;
 
-  // Q^T fragments: chunk (2s + g) of each of this lane's queries
-  u32x4 qf[QG][NQS];
-#pragma unroll
-  for (int qg = 0; qg < QG; ++qg) {
-    const int q = qb * BMQ + (wave * QG + qg) * 32 + col;
+  // Q^T fragments: chunk (2s + g) of this lane's query
+  u32x4 qf[NQS];
+  {
+    const int q = qb * BMQ + wave * 32 + col;
     const int64_t qrow = (int64_t)b * p.Lq + min(q, p.Lq - 1);
 #pragma unroll
     for (int s = 0; s < NQS; ++s)
-      qf[qg][s] = *reinterpret_cast<const u32x4*>(p.Q + qrow * p.ldq + h * DH + (2 * s + g) * VEC);
+      qf[s] = *reinterpret_cast<const u32x4*>(p.Q + qrow * p.ldq + h * DH + (2 * s + g) * VEC);
   }
 
   const T* kbase = p.K + (int64_t)b * p.Lk * p.ldk + h * DH;
@@ -179,26 +177,63 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_
     else load_tail(kt, buf);
   };
 
-  f32x16 o[QG][DH / 32];
+  f32x16 o[DH / 32];
 #pragma unroll
-  for (int qg = 0; qg < QG; ++qg)
+  for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-    for (int dt = 0; dt < DH / 32; ++dt)
+    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+  float l_run = 0.f;
+  const float uscale = SC ? 1.f : p.c;   // MFMA output units -> log2 units
+
+  // S^T of half kk of the tile in buffer buf, plus c0 (an accumulator
+  // initialiser); K fragments are read in batches of KB ahead of their MFMAs.
+  auto scores = [&](int buf, int kk, const f32x16& c0) {
+    constexpr int KB = NQS >= 8 ? NQS / 2 : NQS;
+    f32x16 s = c0;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) o[qg][dt][r] = 0.f;
-  float m_run[QG], l_run[QG];
+    for (int s0 = 0; s0 < NQS; s0 += KB) {
+      u32x4 kf[KB];
 #pragma unroll
-  for (int qg = 0; qg < QG; ++qg) {
-    m_run[qg] = -INFINITY;
-    l_run[qg] = 0.f;
-  }
+      for (int st = 0; st < KB; ++st) kf[st] = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * (s0 + st) + g)];
+#pragma unroll
+      for (int st = 0; st < KB; ++st) Mma<T>::step(s, kf[st], qf[s0 + st]);
+    }
+    return s;
+  };
+  auto mask = [&](f32x16& s, int key) {   // keys >= Lk -> -inf
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (key + 16 * g + r >= p.Lk) s[r] = -INFINITY;
+  };
 
   load_tile(0, 0);
   wait_vmcnt<0>();   // this wave's direct-to-LDS loads have landed
   __syncthreads();   // ... and every other wave's
 
-  for (int kt = 0; kt < ntiles; ++kt) {
-    const int buf = kt & 1;
+  // Initial base: the max of each query's first 32 scores (key 0 exists, so
+  // it is finite).  negm holds -m in MFMA output units.
+  float m_run;
+  f32x16 negm;
+  {
+    f32x16 z;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[r] = 0.f;
+    f32x16 s0 = scores(0, 0, z);
+    if (p.Lk < 32) mask(s0, 0);
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s0[r]);
+    m_run = fmaxf(mx, __shfl_xor(mx, 32)) * uscale;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) negm[r] = -m_run / uscale;
+  }
+
+  // One key tile.  The LDS buffer and whether the tile needs the key-tail
+  // masks are compile-time, so fragment addresses are lane constants plus
+  // immediate offsets and full tiles carry no masking code.
+  auto tile = [&](int kt, auto buf_c, auto masked_c) {
+    constexpr int buf = decltype(buf_c)::value;
+    constexpr bool MASKED = decltype(masked_c)::value;
     // buffer buf^1 was last read before the previous barrier
     if (kt + 1 < ntiles) load_tile(kt + 1, buf ^ 1);
 
@@ -206,21 +241,8 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_
     // the two 32-key halves of the tile in turn: S^T, softmax, O^T += V^T P^T
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      f32x16 s[QG];
-#pragma unroll
-      for (int qg = 0; qg < QG; ++qg)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[qg][r] = 0.f;
-      // every K fragment feeds the QG query groups; all of the half's
-      // fragment reads are issued before its MFMAs
-      u32x4 kf[NQS];
-#pragma unroll
-      for (int st = 0; st < NQS; ++st) kf[st] = ks_[buf][kk * 32 + col][swz<KCH>(col, 2 * st + g)];
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int st = 0; st < NQS; ++st)
-#pragma unroll
-        for (int qg = 0; qg < QG; ++qg) Mma<T>::step(s[qg], kf[st], qf[qg][st]);
+      __builtin_amdgcn_sched_barrier(0);   // halves are not interleaved (register budget)
+      f32x16 s = scores(buf, kk, negm);   // (scores - m) in MFMA output units
       // V^T fragments of this half, in flight during the softmax
       u32x4 vf[NPC][DH / 32];
 #pragma unroll
@@ -229,114 +251,114 @@ __global__ __launch_bounds__(AT_THREADS, QG == 1 ? 8 / AT_WAVES : 1) void flash_
         for (int dt = 0; dt < DH / 32; ++dt)
           vf[u][dt] = vs_[buf][dt * 32 + col][swz<VCH>(col, (kk * 32 + 16 * g) / VEC + u)];
       __builtin_amdgcn_sched_barrier(0);
-      if (key0 + kk * 32 + 32 > p.Lk) {
+      if (MASKED && key0 + kk * 32 + 32 > p.Lk) mask(s, key0 + kk * 32);
+      if constexpr (!SC) {
 #pragma unroll
-        for (int qg = 0; qg < QG; ++qg)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (key0 + kk * 32 + 16 * g + r >= p.Lk) s[qg][r] = -INFINITY;
+        for (int r = 0; r < 16; ++r) s[r] *= uscale;
       }
-      u32x4 pc[QG][NPC];   // P^T chunks, packed as soon as they are computed
+      float mx = -INFINITY;
 #pragma unroll
-      for (int qg = 0; qg < QG; ++qg) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[qg][r]);
-        mx *= p.c;
-        // Lazy rescale: the exponent base m_run (shared by the two lanes of
-        // a query) only moves when a score exceeds it by more than kSlack,
-        // so probabilities stay <= 2^kSlack; numerator and denominator share
-        // the base, so the normalised result is unchanged.  The cross-lane
-        // max is needed only then.  A fully masked sub-tile (mx = -inf)
-        // never moves the base.
-        if (__any(mx > m_run[qg] + kSlack)) {
-          mx = fmaxf(mx, __shfl_xor(mx, 32));
-          const float m_new = fmaxf(m_run[qg], mx);
-          const float alpha = __builtin_amdgcn_exp2f(m_run[qg] - m_new);
-          l_run[qg] *= alpha;
-#pragma unroll
-          for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) o[qg][dt][r] *= alpha;
-          m_run[qg] = m_new;
-        }
-        // lane-partial row sum; the two lanes of a query are combined at the end
-#pragma unroll
-        for (int u = 0; u < NPC; ++u) {
-          float pv[VEC];
-#pragma unroll
-          for (int e = 0; e < VEC; ++e) {
-            pv[e] = __builtin_amdgcn_exp2f(fmaf(s[qg][u * VEC + e], p.c, -m_run[qg]));
-            l_run[qg] += pv[e];
-          }
-          pc[qg][u] = Chunk<T>::pack(pv);
-        }
-      }
-      // every V^T fragment feeds the QG query groups
-#pragma unroll
-      for (int u = 0; u < NPC; ++u)
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
+      // Lazy rescale: the base (shared by the two lanes of a query) only
+      // moves when a score exceeds it by more than kSlack, so probabilities
+      // stay <= 2^kSlack; numerator and denominator share the base, so the
+      // normalised result is unchanged.  The cross-lane max is needed only
+      // then.  A fully masked half (mx = -inf) never moves the base.
+      if (__any(mx > kSlack)) {
+        const float d = fmaxf(fmaxf(mx, __shfl_xor(mx, 32)), 0.f);
+        const float alpha = __builtin_amdgcn_exp2f(-d);
+        l_run *= alpha;
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-          for (int qg = 0; qg < QG; ++qg) Mma<T>::step(o[qg][dt], vf[u][dt], pc[qg][u]);
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          s[r] -= d;
+          negm[r] -= d / uscale;
+        }
+        m_run += d;
+      }
+      // probabilities, packed as the B operand of O^T += V^T P^T; the
+      // lane-partial row sum (lanes l and l^32 are combined at the end)
+      u32x4 pc[NPC];
+#pragma unroll
+      for (int u = 0; u < NPC; ++u) {
+        float pv[VEC];
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) pv[e] = __builtin_amdgcn_exp2f(s[u * VEC + e]);
+        pc[u] = Chunk<T>::pack(pv);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) l_run += pv[e];
+      }
+#pragma unroll
+      for (int u = 0; u < NPC; ++u)
+#pragma unroll
+        for (int dt = 0; dt < DH / 32; ++dt) Mma<T>::step(o[dt], vf[u][dt], pc[u]);
     }
 
     wait_vmcnt<0>();   // tile kt+1 (direct-to-LDS) has landed for this wave
     __syncthreads();
+  };
+  using B0 = std::integral_constant<int, 0>;
+  using B1 = std::integral_constant<int, 1>;
+  const int nfull = p.Lk / AT_BN;   // tiles of 64 valid keys
+  int kt = 0;
+  for (; kt + 2 <= nfull; kt += 2) {
+    tile(kt, B0{}, std::false_type{});
+    tile(kt + 1, B1{}, std::false_type{});
+  }
+  if (kt < nfull) tile(kt++, B0{}, std::false_type{});
+  if (kt < ntiles) {   // the partial last tile
+    if (kt & 1) tile(kt, B1{}, std::true_type{});
+    else tile(kt, B0{}, std::true_type{});
   }
 
+  const int q = qb * BMQ + wave * 32 + col;
+  const float l = l_run + __shfl_xor(l_run, 32);
+  if (q >= p.Lq) return;
+  const float inv = 1.f / l;
+  T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
 #pragma unroll
-  for (int qg = 0; qg < QG; ++qg) {
-    const int q = qb * BMQ + (wave * QG + qg) * 32 + col;
-    const float l = l_run[qg] + __shfl_xor(l_run[qg], 32);
-    if (q >= p.Lq) continue;
-    const float inv = 1.f / l;
-    T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
+  for (int dt = 0; dt < DH / 32; ++dt)
 #pragma unroll
-    for (int dt = 0; dt < DH / 32; ++dt)
+    for (int rr = 0; rr < 4; ++rr) {
+      const int d = dt * 32 + 8 * rr + 4 * g;
+      if constexpr (sizeof(T) == 4) {
+        f32x4 v;
 #pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        const int d = dt * 32 + 8 * rr + 4 * g;
-        if constexpr (sizeof(T) == 4) {
-          f32x4 v;
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rr + e] * inv;
+        *reinterpret_cast<f32x4*>(dst + d) = v;
+      } else {
+        bf16x4 v;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = o[qg][dt][4 * rr + e] * inv;
-          *reinterpret_cast<f32x4*>(dst + d) = v;
-        } else {
-          bf16x4 v;
-#pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[qg][dt][4 * rr + e] * inv);
-          *reinterpret_cast<bf16x4*>(dst + d) = v;
-        }
+        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[dt][4 * rr + e] * inv);
+        *reinterpret_cast<bf16x4*>(dst + d) = v;
       }
-  }
+    }
 }
 
-#ifndef DIF_ATTN_QG
-#define DIF_ATTN_QG 1
-#endif
-
 template <typename T, int DH>
-void launch_dh(const AttnParams<T>& p, hipStream_t stream) {
-  // query groups per wave: one (two waves per SIMD hide the softmax behind
-  // the other wave's MFMAs better than the halved LDS traffic of two groups)
-  constexpr int QG = (sizeof(T) == 2 && DH == 128) ? DIF_ATTN_QG : 1;
-  constexpr int BMQ = AT_WAVES * 32 * QG;
+void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
+  constexpr int BMQ = AT_WAVES * 32;
   const int blocks = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
-  hipLaunchKernelGGL((flash_attn_kernel<T, DH, QG>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
+  if (q_scaled)
+    hipLaunchKernelGGL((flash_attn_kernel<T, DH, true>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
+  else
+    hipLaunchKernelGGL((flash_attn_kernel<T, DH, false>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
 }
 
 template <typename T>
 hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                             const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk,
-                            int H, hipStream_t stream) {
+                            int H, hipStream_t stream, bool q_scaled) {
   if (B <= 0 || Lq <= 0 || H <= 0) return hipSuccess;
   AttnParams<T> p{Q, K, Vt, O, ldq, ldk, ldvt, ldo, B, Lq, Lk, H,
                   1.4426950408889634f / sqrtf((float)head_dim)};
   if (head_dim == 128) {
-    launch_dh<T, 128>(p, stream);
+    launch_dh<T, 128>(p, q_scaled, stream);
   } else if (head_dim == 64) {
-    launch_dh<T, 64>(p, stream);
+    launch_dh<T, 64>(p, q_scaled, stream);
   } else {
     return hipErrorInvalidValue;
   }
@@ -345,9 +367,9 @@ hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, i
 
 template hipError_t launch_attention<bf16>(int, const bf16*, int64_t, const bf16*, int64_t,
                                            const bf16*, int64_t, bf16*, int64_t, int, int, int,
-                                           int, hipStream_t);
+                                           int, hipStream_t, bool);
 template hipError_t launch_attention<float>(int, const float*, int64_t, const float*, int64_t,
                                             const float*, int64_t, float*, int64_t, int, int,
-                                            int, int, hipStream_t);
+                                            int, int, hipStream_t, bool);
 
 }  // namespace dif

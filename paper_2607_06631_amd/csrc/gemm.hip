@@ -34,14 +34,19 @@ constexpr int BN_MAX = 256; // largest workgroup tile width over the shapes belo
 enum { GA_NONE = 0, GA_ROWS = 1, GA_KCH = 2 };
 constexpr uint32_t kMasked = 0x80000000u;  // buffer offset beyond any descriptor range
 
+// Up to three B matrices ("segments", e.g. the q, k and v weights) share A
+// and one launch; segment s writes output columns [s*N, (s+1)*N).
+constexpr int kMaxSeg = 3;
+
 template <typename T, typename OutT>
 struct GemmParams {
   const T* A;
-  const T* B;
+  const T* Bs[kMaxSeg];
   OutT* C;
   int64_t lda, ldb, ldc;
   int M, N, K;
-  const float* bias;
+  const float* biases[kMaxSeg];
+  int nseg;
   const float* gate0;
   const float* gate1;
   const int32_t* rows;   // GA_ROWS
@@ -67,16 +72,22 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   const int g = lane >> 5, col = lane & 31;
 
   // logical tile: XCD-contiguous ranges, then groups of GM row-tiles that
-  // walk the N tiles together (operand reuse in L2)
+  // walk the N tiles of all segments together (operand reuse in L2)
   const int nbm = (p.M + BM - 1) / BM, nbn = (p.N + BN - 1) / BN;
-  const int bid = xcd_remap(blockIdx.x, nbm * nbn);
+  const int nbv = nbn * p.nseg;
+  const int bid = xcd_remap(blockIdx.x, nbm * nbv);
   constexpr int GM = 8;
-  const int group = bid / (GM * nbn);
+  const int group = bid / (GM * nbv);
   const int first_m = group * GM;
   const int gsize = min(nbm - first_m, GM);
-  const int in_group = bid - group * GM * nbn;
+  const int in_group = bid - group * GM * nbv;
   const int m0 = (first_m + in_group % gsize) * BM;
-  const int n0 = (in_group / gsize) * BN;
+  const int nt = in_group / gsize;
+  const int sg = nt / nbn;
+  const int n0 = (nt - sg * nbn) * BN;
+  const T* Bsg = p.Bs[sg];
+  const float* bias_sg = p.biases[sg];
+  OutT* Csg = p.C + (int64_t)sg * p.N;
 
   // global -> LDS staging: thread loads chunk lc of rows lr + RPL * i with
   // buffer loads against block-local descriptors; rows past M / N fall
@@ -88,7 +99,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   const uint32_t b_bytes =
       GA == GA_ROWS ? (uint32_t)((int64_t)p.b_rows * p.ldb * (int64_t)sizeof(T))
                     : (uint32_t)(min(BN, p.N - n0) * p.ldb * (int64_t)sizeof(T));
-  const T* b_base = GA == GA_ROWS ? p.B : p.B + (int64_t)n0 * p.ldb;
+  const T* b_base = GA == GA_ROWS ? Bsg : Bsg + (int64_t)n0 * p.ldb;
   const __amdgpu_buffer_rsrc_t a_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<T*>(p.A + (int64_t)m0 * p.lda), (short)0, a_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t b_rsrc =
@@ -121,13 +132,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   // Two register staging sets: tile kt+2 is requested while tile kt is
   // computed, so global latency is hidden behind two compute phases.
   u32x4 ra0[LA], rb0[LB], ra1[LA], rb1[LB];
+  // GA_KCH: byte offset of this thread's chunk for the next tile to load,
+  // read from LDS one k-tile ahead so the loads never wait on it
+  uint32_t kb = 0;
+  auto kb_fetch = [&](int kt) {
+    if constexpr (GA == GA_KCH) {
+      if (kt < nk) kb = kch_lds[kt * G_CH + lc];
+    }
+  };
   auto gload = [&](int kt, u32x4* ra, u32x4* rb) {
     const int koff = kt * BK * (int)sizeof(T);
 #pragma unroll
     for (int i = 0; i < LA; ++i)
       ra[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_off[i], koff, 0));
     if constexpr (GA == GA_KCH) {
-      const uint32_t kb = kch_lds[kt * G_CH + lc];
 #pragma unroll
       for (int i = 0; i < LB; ++i)
         rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i] + kb, 0, 0));
@@ -178,14 +196,20 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   auto ktile = [&](int kt, u32x4* ra_cur, u32x4* rb_cur, u32x4* ra_nxt, u32x4* rb_nxt) {
     __syncthreads();
     if (kt + 1 < nk) sstore((kt + 1) & 1, ra_cur, rb_cur);
-    if (kt + 2 < nk) gload(kt + 2, ra_nxt, rb_nxt);
+    if (kt + 2 < nk) {
+      gload(kt + 2, ra_nxt, rb_nxt);
+      kb_fetch(kt + 3);
+    }
     compute(kt & 1);
   };
 
   if (nk > 0) {
+    kb_fetch(0);
     gload(0, ra0, rb0);
     sstore(0, ra0, rb0);
+    kb_fetch(1);
     if (nk > 1) gload(1, ra1, rb1);
+    kb_fetch(2);
   }
   int kt = 0;
   for (; kt + 1 < nk; kt += 2) {
@@ -203,9 +227,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
     float bias = 0.f;
     if constexpr (GA == GA_ROWS) {
       const int r = p.rows[n];
-      if (p.bias && r >= 0) bias = p.bias[r];
+      if (bias_sg && r >= 0) bias = bias_sg[r];
     } else {
-      if (p.bias) bias = p.bias[n];
+      if (bias_sg) bias = bias_sg[n];
     }
     float gate = 1.f;
     if (EPI == EPI_RESIDUAL && p.gate0) gate = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
@@ -215,7 +239,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + wm * TM * 32 + i * 32 + acc_row(r, g);
         if (m < p.M) {
-          OutT* dst = p.C + (int64_t)m * p.ldc + n;
+          OutT* dst = Csg + (int64_t)m * p.ldc + n;
           const float v = acc[i][j][r] + bias;
           if (EPI == EPI_STORE) {
             *dst = from_f32<OutT>(v);
@@ -247,7 +271,7 @@ void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
   constexpr int WGM = 2, WGN = 4, TM = 4, TN = 2;
 #endif
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
-  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN);
+  const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.nseg;
   const size_t dyn = GA == GA_KCH ? (size_t)(p.K / Chunk<T>::VEC) * sizeof(uint32_t) : 0;
   hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI, GA, WGM, WGN, TM, TN>), dim3(tiles),
                      dim3(64 * WGM * WGN), dyn, stream, p);
@@ -258,8 +282,29 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
                        const float* gate1, hipStream_t stream, const GemmGather* gather) {
   if (M <= 0 || N <= 0) return hipSuccess;
-  GemmParams<T, OutT> p{A, B, C, lda, ldb, ldc, M, N, K, bias, gate0, gate1, nullptr, nullptr, 0};
-  if (!gather || (!gather->rows && !gather->kchunks)) {
+  GemmParams<T, OutT> p{};
+  p.A = A;
+  p.Bs[0] = B;
+  p.C = C;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.biases[0] = bias;
+  p.nseg = 1;
+  p.gate0 = gate0;
+  p.gate1 = gate1;
+  if (gather && gather->nseg > 1) {
+    if (gather->nseg > kMaxSeg || epi == EPI_RESIDUAL) return hipErrorInvalidValue;
+    p.nseg = gather->nseg;
+    for (int sg = 1; sg < p.nseg; ++sg) {
+      p.Bs[sg] = static_cast<const T*>(gather->seg_b[sg - 1]);
+      p.biases[sg] = gather->seg_bias[sg - 1];
+    }
+  }
+  if (!gather || (!gather->rows && !gather->kchunks)) {  // (segments allowed)
     switch (epi) {
       case EPI_STORE: launch_tile<T, OutT, EPI_STORE, GA_NONE>(p, stream); break;
       case EPI_GELU: launch_tile<T, OutT, EPI_GELU, GA_NONE>(p, stream); break;

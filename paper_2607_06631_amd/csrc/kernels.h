@@ -16,10 +16,16 @@ enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESIDUAL = 2 };
 //   kchunks: for each 16-byte chunk c of the K extent, the chunk of every B
 //            row it is read from (-1: zeros); at most 8192 chunks.  Epilogue
 //            RESIDUAL.  A operand columns are compacted as K.
+//   nseg > 1: B (and bias) of segments 1.. come from seg_b / seg_bias; the
+//            segments share A and the row table, segment s writes C columns
+//            [s*N, (s+1)*N).  Epilogues STORE and GELU.
 struct GemmGather {
   const int32_t* rows;
   const int32_t* kchunks;
   int b_rows;
+  int nseg = 1;
+  const void* seg_b[2] = {nullptr, nullptr};
+  const float* seg_bias[2] = {nullptr, nullptr};
 };
 
 // C[M,N] = epi(A[M,K] * B[N,K]^T); T in {float, __bf16}; OutT in {T, float}.
@@ -29,10 +35,11 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
                        const float* gate1, hipStream_t stream, const GemmGather* gather = nullptr);
 
 // Flash attention; V given transposed (see dif_attention in dif.h).
+// q_scaled: Q already multiplied by log2(e)/sqrt(head_dim).
 template <typename T>
 hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                             const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk,
-                            int H, hipStream_t stream);
+                            int H, hipStream_t stream, bool q_scaled = false);
 
 // Row LayerNorm of x [M, D] then
 //   mode 0: y = xhat * (1 + p2 + p3) + (p0 + p1)      (AdaLN; p1/p3 may be null)
@@ -44,7 +51,7 @@ hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0
 
 // In place on rows of buf (stride ld): for each of nseg segments of width a
 // at column offset off[s]: y = x / sqrt(sum(x^2) * inv_norm_dim + eps) * gain[s][idx[c]]
-// (idx null: identity),
+// (idx null: identity), times scale0 on segment 0,
 // then (rope != null) rotate consecutive pairs of each head_dim-wide head by
 // the token's 3D angles.
 struct RopeDesc {
@@ -58,7 +65,7 @@ template <typename T>
 hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off0, int off1,
                           const float* g0, const float* g1, float inv_norm_dim, float eps,
                           const RopeDesc* rope, hipStream_t stream,
-                          const int32_t* gain_idx = nullptr);
+                          const int32_t* gain_idx = nullptr, float scale0 = 1.f);
 
 // Vt[(b*a + c)*ldvt + j] = src[(b*Lk + j)*lds + c] for j < Lk, 0 for Lk <= j < ldvt.
 template <typename T>

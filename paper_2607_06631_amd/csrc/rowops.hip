@@ -116,14 +116,14 @@ template <typename T>
 __global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
                                                             int nseg, int off0, int off1,
                                                             const float* g0, const float* g1,
-                                                            const int32_t* gidx, float inv_dim,
-                                                            float eps, RopeDesc rope) {
+                                                            const int32_t* gidx, float scale0,
+                                                            float inv_dim, float eps, RopeDesc rope) {
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int NP = VEC / 2;  // pairs per chunk
   extern __shared__ float gain_lds[];  // [nseg][a]
   for (int n = threadIdx.x; n < a; n += R_THREADS) {
     const int gn = gidx ? gidx[n] : n;
-    gain_lds[n] = g0[gn];
+    gain_lds[n] = g0[gn] * scale0;
     if (nseg > 1) gain_lds[a + n] = g1[gn];
   }
   __syncthreads();
@@ -200,7 +200,8 @@ __global__ __launch_bounds__(R_THREADS) void qk_norm_kernel(T* buf, int64_t ld, 
 template <typename T>
 hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off0, int off1,
                           const float* g0, const float* g1, float inv_norm_dim, float eps,
-                          const RopeDesc* rope, hipStream_t stream, const int32_t* gain_idx) {
+                          const RopeDesc* rope, hipStream_t stream, const int32_t* gain_idx,
+                          float scale0) {
   if (rows <= 0 || a <= 0) return hipSuccess;
   RopeDesc rd{};
   if (rope) rd = *rope;
@@ -209,7 +210,7 @@ hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off
   if ((64 * VEC) % rd.head_dim != 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL((qk_norm_kernel<T>), dim3((rows + R_ROWS - 1) / R_ROWS), dim3(R_THREADS),
                      nseg * a * sizeof(float), stream, buf, ld, rows, a, nseg, off0, off1, g0, g1,
-                     gain_idx, inv_norm_dim, eps, rd);
+                     gain_idx, scale0, inv_norm_dim, eps, rd);
   return hipGetLastError();
 }
 
@@ -365,7 +366,7 @@ hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream) 
                                      const float*, const float*, float, hipStream_t);          \
   template hipError_t launch_qk_norm<T>(T*, int64_t, int, int, int, int, int, const float*,    \
                                         const float*, float, float, const RopeDesc*,           \
-                                        hipStream_t, const int32_t*);                          \
+                                        hipStream_t, const int32_t*, float);                   \
   template hipError_t launch_transpose_vt<T>(const T*, int64_t, int, int, int, T*, int64_t,    \
                                              hipStream_t);                                     \
   template hipError_t launch_gather<T>(const T*, int64_t, T*, int64_t, int, int,               \
