@@ -229,6 +229,38 @@ dif_status dif_step_forward(const dif_plan* plan, const float* z, float t, const
 dif_status dif_euler(float* z, const float* v, float sigma_from, float sigma_to, int64_t n,
                      dif_stream stream);
 
+/* Clean-estimate and re-noise update between sampler steps (the student's
+ * single-step clean prediction and the re-noising of Sec. 3.1 / Sec. 4.2,
+ * with sigma = 1 - tau), in place on n float32 elements:
+ *   x_hat = z - sigma_from * v;   z = (1 - sigma_to) * x_hat + sigma_to * eps.
+ * eps (device, n float32, caller-drawn noise) may be null only when
+ * sigma_to == 0, which leaves z = x_hat.  Errors: DIF_E_ARG (null z / v,
+ * non-finite sigma_from, sigma_to outside [0, 1], eps missing), DIF_E_SHAPE
+ * (n < 0), DIF_E_HIP. */
+dif_status dif_renoise(float* z, const float* v, float sigma_from, float sigma_to, const float* eps,
+                       int64_t n, dif_stream stream);
+
+#define DIF_SAMPLER_EULER 0   /* z += (sigma_{s+1} - sigma_s) v                         */
+#define DIF_SAMPLER_RENOISE 1 /* x_hat = z - sigma_s v; z = (1 - sigma_{s+1}) x_hat + sigma_{s+1} eps_s */
+
+/* The student applied step after step from its current state to the last
+ * step (the output rollout of Sec. 4.2 and Fig. 2(b)): for i < n_steps,
+ * v = step(plans[i], z, timesteps[i]) then the sampler update from
+ * sigma = timesteps[i] / 1000 to timesteps[i+1] / 1000 (0 after the last).
+ * The last update of either sampler leaves the clean estimate z - sigma v.
+ * Start mid-chain by passing the remaining plans and timesteps.  eps[i]
+ * (device, B*L*patch_dim float32) is the re-noise of transition i, needed
+ * for i < n_steps - 1 with DIF_SAMPLER_RENOISE (eps itself may be null for
+ * DIF_SAMPLER_EULER).  z [B, L, Cp] float32 in place; v_scratch: device
+ * float32 of the same size; ctx, ws, ws_bytes, B, L, Lc as for
+ * dif_step_forward.  Everything is enqueued on `stream`.  Errors: those of
+ * dif_step_forward and dif_renoise, DIF_E_ARG for null plans / timesteps,
+ * unknown sampler, plans of different models. */
+dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
+                       int32_t sampler, float* z, const float* const* eps, const void* ctx,
+                       int32_t B, int32_t L, int32_t Lc, float* v_scratch, void* ws,
+                       size_t ws_bytes, dif_stream stream);
+
 /* ------------------------------------------------------------------------
  * Operator-level entry points: the hot kernels on their own, for tests and
  * benchmarks of a single kernel.

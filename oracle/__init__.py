@@ -15,5 +15,5 @@ readings taken where the paper is silent.
 from .dit import (  # noqa: F401
     sinusoid, silu, gelu_tanh, layer_norm, rms_norm, rope_split, rope_angles,
     apply_rope, softmax_rows, attention, apply_keep, time_embedding, block,
-    step, euler, denoise, sigmas,
+    step, euler, denoise, sigmas, predict_clean, renoise, rollout,
 )

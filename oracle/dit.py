@@ -266,6 +266,38 @@ def euler(z, v, sigma_from: float, sigma_to: float):
     return z + (sigma_to - sigma_from) * v
 
 
+def predict_clean(z, v, sigma: float):
+    """Clean-data estimate from the model prediction at noise level sigma
+    (the single-step prediction of Sec. 4.2).  With z = (1 - sigma) x +
+    sigma eps and v = eps - x (R7) this is x."""
+    return z - sigma * v
+
+
+def renoise(x_hat, sigma_to: float, eps):
+    """Re-noise a clean estimate to level sigma_to with noise eps (the
+    re-noising of Sec. 3.1, written in sigma = 1 - tau)."""
+    return (1.0 - sigma_to) * x_hat + sigma_to * eps
+
+
+def rollout(z, ctx, w: dict, masks_per_step, cfg, eps_per_step=None, start: int = 0,
+            sampler: str = "renoise", dtype=np.float64):
+    """Sequential denoise from step `start` to the last step (the output
+    rollout of Sec. 4.2 / Fig. 2(b)).  sampler "euler": z += dsigma v;
+    "renoise": x_hat = z - sigma_s v, then z = (1 - sigma_{s+1}) x_hat +
+    sigma_{s+1} eps_s; the last step returns x_hat (sigma after it is 0)."""
+    z = np.asarray(z, dtype=dtype)
+    sig = sigmas(cfg.timesteps)
+    T = len(cfg.timesteps)
+    for s in range(start, T):
+        v = step(z, cfg.timesteps[s], ctx, w, masks_per_step[s], cfg, dtype)
+        if sampler == "euler":
+            z = euler(z, v, sig[s], sig[s + 1])
+        else:
+            x_hat = predict_clean(z, v, sig[s])
+            z = x_hat if s + 1 == T else renoise(x_hat, sig[s + 1], np.asarray(eps_per_step[s], dtype))
+    return z
+
+
 def denoise(z, ctx, w: dict, masks_per_step, cfg, dtype=np.float64):
     """Run the T-step sampler; step s uses its own structure masks_per_step[s]."""
     z = np.asarray(z, dtype=dtype)

@@ -94,6 +94,9 @@ def lib():
             "dif_block_forward": (i32, [vp, i32, vp, vp, vp, i32, i32, i32, vp, sz, vp]),
             "dif_step_forward": (i32, [vp, vp, f32, vp, i32, i32, i32, vp, vp, sz, vp]),
             "dif_euler": (i32, [vp, vp, f32, f32, i64, vp]),
+            "dif_renoise": (i32, [vp, vp, f32, f32, vp, i64, vp]),
+            "dif_rollout": (i32, [C.POINTER(vp), C.POINTER(f32), i32, i32, vp, C.POINTER(vp), vp,
+                                  i32, i32, i32, vp, vp, sz, vp]),
             "dif_gemm": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp, vp, vp, vp]),
             "dif_attention": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp]),
             "dif_profile_enable": (i32, [i32]),
@@ -294,6 +297,29 @@ def dif_step_forward(plan: Plan, z, t: float, ctx, v_out, ws, stream=None) -> No
     Lc = ctx.shape[1]
     _check(lib().dif_step_forward(plan.handle, _ptr(z), float(t), _ptr(ctx), B, L, Lc, _ptr(v_out),
                                   _ptr(ws), ws.numel(), _stream(stream)))
+
+
+DIF_SAMPLER_EULER, DIF_SAMPLER_RENOISE = 0, 1
+SAMPLERS = {"euler": DIF_SAMPLER_EULER, "renoise": DIF_SAMPLER_RENOISE}
+
+
+def dif_renoise(z, v, sigma_from: float, sigma_to: float, eps=None, stream=None) -> None:
+    _check(lib().dif_renoise(_ptr(z), _ptr(v), float(sigma_from), float(sigma_to),
+                             _ptr(eps) if eps is not None else None, z.numel(), _stream(stream)))
+
+
+def dif_rollout(plans, timesteps, z, ctx, v_scratch, ws, eps=None, sampler: str = "renoise",
+                stream=None) -> None:
+    """Steps plans[0..] from z (in place) to the clean estimate of the last one."""
+    n = len(plans)
+    P = (C.c_void_p * n)(*[p.handle for p in plans])
+    ts = (C.c_float * n)(*[float(t) for t in timesteps])
+    E = None
+    if eps is not None:
+        E = (C.c_void_p * n)(*[(_ptr(e) if e is not None else None) for e in eps])
+    B, L = z.shape[0], z.shape[1]
+    _check(lib().dif_rollout(P, ts, n, SAMPLERS[sampler], _ptr(z), E, _ptr(ctx), B, L, ctx.shape[1],
+                             _ptr(v_scratch), _ptr(ws), ws.numel(), _stream(stream)))
 
 
 def dif_euler(z, v, sigma_from: float, sigma_to: float, stream=None) -> None:

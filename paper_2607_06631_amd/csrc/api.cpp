@@ -914,6 +914,52 @@ dif_status dif_euler(float* z, const float* v, float sigma_from, float sigma_to,
   GUARD_END
 }
 
+dif_status dif_renoise(float* z, const float* v, float sigma_from, float sigma_to, const float* eps,
+                       int64_t n, dif_stream stream) {
+  GUARD_BEGIN
+  if (!z || !v) return fail(DIF_E_ARG, "null argument");
+  if (n < 0) return fail(DIF_E_SHAPE, "n < 0");
+  if (!std::isfinite(sigma_from) || !std::isfinite(sigma_to) || sigma_to < 0.f || sigma_to > 1.f)
+    return fail(DIF_E_ARG, "sigma_from must be finite and 0 <= sigma_to <= 1");
+  if (sigma_to != 0.f && !eps) return fail(DIF_E_ARG, "eps is null but sigma_to = %g", sigma_to);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  ProfScope ps(PK_ELEMENTWISE, s, 4.0 * n, (sigma_to != 0.f ? 16.0 : 12.0) * n);
+  HIP_TRY(dif::launch_renoise(z, v, sigma_from, sigma_to, sigma_to != 0.f ? eps : nullptr, n, s));
+  return DIF_OK;
+  GUARD_END
+}
+
+dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
+                       int32_t sampler, float* z, const float* const* eps, const void* ctx,
+                       int32_t B, int32_t L, int32_t Lc, float* v_scratch, void* ws,
+                       size_t ws_bytes, dif_stream stream) {
+  GUARD_BEGIN
+  if (!plans || !timesteps || !z || !ctx || !v_scratch) return fail(DIF_E_ARG, "null argument");
+  if (n_steps < 1) return fail(DIF_E_ARG, "n_steps must be >= 1");
+  if (sampler != DIF_SAMPLER_EULER && sampler != DIF_SAMPLER_RENOISE)
+    return fail(DIF_E_ARG, "unknown sampler %d", sampler);
+  for (int i = 0; i < n_steps; ++i) {
+    if (!plans[i]) return fail(DIF_E_ARG, "plan %d is null", i);
+    if (plans[i]->model != plans[0]->model) return fail(DIF_E_ARG, "plans of different models");
+    if (!std::isfinite(timesteps[i])) return fail(DIF_E_ARG, "timestep %d is not finite", i);
+    if (sampler == DIF_SAMPLER_RENOISE && i + 1 < n_steps && (!eps || !eps[i]))
+      return fail(DIF_E_ARG, "re-noise sampler needs eps[%d]", i);
+  }
+  const int64_t n = (int64_t)B * L * plans[0]->model->cfg.patch_dim;
+  for (int i = 0; i < n_steps; ++i) {
+    DIF_TRY(dif_step_forward(plans[i], z, timesteps[i], ctx, B, L, Lc, v_scratch, ws, ws_bytes,
+                             stream));
+    const float sf = timesteps[i] / 1000.f;
+    const float st = i + 1 < n_steps ? timesteps[i + 1] / 1000.f : 0.f;
+    if (sampler == DIF_SAMPLER_EULER)
+      DIF_TRY(dif_euler(z, v_scratch, sf, st, n, stream));
+    else
+      DIF_TRY(dif_renoise(z, v_scratch, sf, st, i + 1 < n_steps ? eps[i] : nullptr, n, stream));
+  }
+  return DIF_OK;
+  GUARD_END
+}
+
 dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda, const void* B,
                     int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K,
                     int32_t epilogue, const float* bias, const float* gate0, const float* gate1,

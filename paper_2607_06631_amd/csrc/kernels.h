@@ -86,6 +86,9 @@ hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out
 hipError_t launch_sinusoid(float t, int dim, float* out, hipStream_t stream);
 hipError_t launch_silu(const float* x, float* y, int n, hipStream_t stream);
 hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStream_t stream);
+// z = (1 - sigma_to) (z - sigma_from v) + sigma_to eps; eps null means sigma_to = 0.
+hipError_t launch_renoise(float* z, const float* v, float sigma_from, float sigma_to,
+                          const float* eps, int64_t n, hipStream_t stream);
 template <typename T>
 hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream);
 

@@ -346,6 +346,25 @@ hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStre
   return hipGetLastError();
 }
 
+// z = (1 - st) * (z - sf * v) + st * eps   (eps unused when st == 0)
+__global__ void renoise_kernel(float* z, const float* v, float sf, float st, const float* eps,
+                               int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const float x = fmaf(-sf, v[i], z[i]);
+    z[i] = eps ? fmaf(st, eps[i], (1.f - st) * x) : x;
+  }
+}
+
+hipError_t launch_renoise(float* z, const float* v, float sigma_from, float sigma_to,
+                          const float* eps, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((n + 255) / 256, 65536);
+  hipLaunchKernelGGL(renoise_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, z, v, sigma_from,
+                     sigma_to, eps, n);
+  return hipGetLastError();
+}
+
 template <typename T>
 __global__ void cast_kernel(const float* src, T* dst, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;

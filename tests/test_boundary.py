@@ -100,3 +100,21 @@ def test_op_entry_points_reject_bad_arguments(lib):
     assert lib.dif_model_create(None, None, None) == -1
     info = B.DifLayerInfo()
     assert lib.dif_plan_layer_info(None, 0, C.byref(info)) == -1
+
+
+def test_sampler_entry_points_reject_bad_arguments(lib):
+    # validation happens before any pointer is touched or kernel launched
+    dummy = C.c_void_p(256)
+    assert lib.dif_renoise(dummy, dummy, 0.75, 0.5, None, 4, None) == -1   # eps needed
+    assert lib.dif_renoise(dummy, dummy, 0.75, 1.5, dummy, 4, None) == -1  # sigma_to > 1
+    assert lib.dif_renoise(dummy, dummy, float("nan"), 0.0, None, 4, None) == -1
+    assert lib.dif_renoise(dummy, dummy, 0.75, 0.0, None, -1, None) == -2
+    assert lib.dif_renoise(None, dummy, 0.75, 0.0, None, 4, None) == -1
+    P = (C.c_void_p * 1)(None)
+    ts = (C.c_float * 1)(999.0)
+    args = (dummy, None, dummy, 1, 16, 16, dummy, dummy, 0, None)
+    assert lib.dif_rollout(P, ts, 0, 1, *args) == -1     # n_steps < 1
+    assert lib.dif_rollout(P, ts, 1, 7, *args) == -1     # unknown sampler
+    assert lib.dif_rollout(P, ts, 1, 1, *args) == -1     # null plan
+    assert b"plan 0" in lib.dif_last_error()
+    assert lib.dif_plan_bytes_ex(None, None, 0, None) == -1

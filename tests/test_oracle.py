@@ -431,3 +431,54 @@ def test_full_denoise_runs_and_is_finite():
     # float32 and float64 oracles agree to float32 rounding
     out32 = O.denoise(z, ctx, w, masks, cfg, dtype=np.float32)
     assert np.max(np.abs(out32 - out)) / np.max(np.abs(out)) < 1e-5
+
+
+def test_renoise_sampler_on_the_exact_flow():
+    """On the straight path z_sigma = (1 - sigma) x + sigma eps with the exact
+    velocity v = eps - x (R7): the clean estimate is x at every level,
+    re-noising with the same eps lands on the path, and it coincides with
+    the Euler step; to sigma = 0 both give x."""
+    g = np.random.default_rng(5)
+    x, eps = g.standard_normal(64), g.standard_normal(64)
+    v = eps - x
+    for s_from, s_to in [(0.999, 0.75), (0.75, 0.5), (0.25, 0.0)]:
+        z = (1 - s_from) * x + s_from * eps
+        np.testing.assert_allclose(O.predict_clean(z, v, s_from), x, rtol=0, atol=1e-12)
+        on_path = (1 - s_to) * x + s_to * eps
+        np.testing.assert_allclose(O.renoise(O.predict_clean(z, v, s_from), s_to, eps), on_path,
+                                   rtol=0, atol=1e-12)
+        np.testing.assert_allclose(O.euler(z, v, s_from, s_to), on_path, rtol=0, atol=1e-12)
+    # a different eps moves the re-noised point by sigma_to (eps' - eps) only
+    eps2 = g.standard_normal(64)
+    z = 0.25 * x + 0.75 * eps
+    np.testing.assert_allclose(O.renoise(O.predict_clean(z, v, 0.75), 0.5, eps2) -
+                               O.euler(z, v, 0.75, 0.5), 0.5 * (eps2 - eps), rtol=0, atol=1e-12)
+
+
+def test_rollout_samplers_and_start_step():
+    """Both samplers end with the clean estimate of the last step; the Euler
+    rollout is the plain denoise; a rollout started at step s equals steps
+    s.. of the full chain fed the same intermediate latent."""
+    cfg = MICRO
+    w = synth.make_weights(cfg, seed=2)
+    masks = [synth.make_masks(cfg, s) for s in range(4)]
+    z = synth.make_latents(cfg, seed=6)
+    ctx = synth.make_context(cfg, seed=6)
+    g = np.random.default_rng(7)
+    eps = [g.standard_normal(z.shape) for _ in range(4)]
+    np.testing.assert_array_equal(O.rollout(z, ctx, w, masks, cfg, sampler="euler"),
+                                  O.denoise(z, ctx, w, masks, cfg))
+    # one step by hand, then the rest through rollout(start=1)
+    sig = O.sigmas(cfg.timesteps)
+    v0 = O.step(z, cfg.timesteps[0], ctx, w, masks[0], cfg)
+    z1 = O.renoise(O.predict_clean(z, v0, sig[0]), sig[1], eps[0])
+    full = O.rollout(z, ctx, w, masks, cfg, eps, sampler="renoise")
+    np.testing.assert_allclose(O.rollout(z1, ctx, w, masks, cfg, eps, start=1), full,
+                               rtol=0, atol=1e-12)
+    # the last step returns z - sigma_T v regardless of the sampler
+    z3 = synth.make_latents(cfg, seed=8)
+    v3 = O.step(z3, cfg.timesteps[3], ctx, w, masks[3], cfg)
+    np.testing.assert_allclose(O.rollout(z3, ctx, w, masks, cfg, eps, start=3),
+                               z3 - sig[3] * v3, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(O.rollout(z3, ctx, w, masks, cfg, start=3, sampler="euler"),
+                               z3 - sig[3] * v3, rtol=0, atol=1e-12)

@@ -116,6 +116,14 @@ def make_latents(cfg: Config, seed: int = 0) -> np.ndarray:
     return g.standard_normal((cfg.batch, cfg.seq_len, cfg.patch_dim), dtype=np.float32)
 
 
+def make_renoise_eps(cfg: Config, seed: int = 0) -> List[np.ndarray]:
+    """Noise drawn for the re-noise sampler, one latent-shaped array per step
+    transition (the method's random draws, passed in as inputs)."""
+    return [rng(SEED_INPUTS, seed, cfg.name, "eps", s).standard_normal(
+        (cfg.batch, cfg.seq_len, cfg.patch_dim), dtype=np.float32)
+        for s in range(len(cfg.timesteps) - 1)]
+
+
 def make_context(cfg: Config, seed: int = 0, text_len: Optional[int] = None) -> np.ndarray:
     Lc = cfg.text_len if text_len is None else text_len
     g = rng(SEED_INPUTS, seed, cfg.name, "ctx")
