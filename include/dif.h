@@ -261,6 +261,40 @@ dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int
                        int32_t B, int32_t L, int32_t Lc, float* v_scratch, void* ws,
                        size_t ws_bytes, dif_stream stream);
 
+/* Hard gates of one step from its continuous masks (Sec. 4.1): block gate
+ * 1 iff m_block[l] > 0; a head is kept iff the mean of its head_dim mask
+ * values is > 0 (summed in double, in index order); FFN channels form
+ * consecutive chunks of `chunk` (the paper uses C = 8) and chunk c of layer
+ * l is kept iff m_ffn[l * (ffn_dim / chunk) + c] > 0.  Comparisons are
+ * strict, so 0 (and NaN) prunes.  Host memory, no HIP call:
+ *   m_block [n_layers], m_self / m_cross [n_layers * dim] (head h owns
+ *   entries h*head_dim ..), m_ffn [n_layers * ffn_dim / chunk] float32 in;
+ *   block_keep [n_layers], self_head_keep / cross_head_keep
+ *   [n_layers * n_heads], ffn_keep [n_layers * ffn_dim] uint8 out — the
+ *   dif_step_masks arrays of that step.
+ * Errors: those of dif_validate_config, DIF_E_ARG (null), DIF_E_SHAPE
+ * (chunk < 1 or ffn_dim not a multiple of chunk). */
+dif_status dif_hard_gates(const dif_config* cfg, int32_t chunk, const float* m_block,
+                          const float* m_self, const float* m_cross, const float* m_ffn,
+                          uint8_t* block_keep, uint8_t* self_head_keep, uint8_t* cross_head_keep,
+                          uint8_t* ffn_keep);
+
+/* FFN channel reordering before chunking (App. A): sorts layer `layer`'s
+ * hidden channels by decreasing L2 norm of their weights — W1 row, b1 entry
+ * and W2 column, norms in double, ties in index order — and writes the
+ * permuted W1 rows to w1_out [ffn_dim, dim], b1 to b1_out [ffn_dim] and W2
+ * columns to w2_out [dim, ffn_dim] (device, caller-owned, model dtype /
+ * float32), and the permutation to perm_out [ffn_dim] (host: channel i of
+ * the outputs is channel perm_out[i] of the model).  Permuting the three
+ * together leaves the block's function unchanged, so the outputs can stand
+ * in for the layer's FFN weights in a new model.  scratch: device memory of
+ * >= ffn_dim * 12 bytes, 8-byte aligned.  The model's weights are only
+ * read.  The call synchronises `stream` (the sort runs on the host).
+ * Errors: DIF_E_ARG (null, layer out of range), DIF_E_WORKSPACE, DIF_E_HIP. */
+dif_status dif_ffn_reorder(const dif_model* model, int32_t layer, void* w1_out, float* b1_out,
+                           void* w2_out, int32_t* perm_out, void* scratch, size_t scratch_bytes,
+                           dif_stream stream);
+
 /* ------------------------------------------------------------------------
  * Operator-level entry points: the hot kernels on their own, for tests and
  * benchmarks of a single kernel.

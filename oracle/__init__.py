@@ -17,3 +17,4 @@ from .dit import (  # noqa: F401
     apply_rope, softmax_rows, attention, apply_keep, time_embedding, block,
     step, euler, denoise, sigmas, predict_clean, renoise, rollout,
 )
+from .gates import hard_gates, ffn_channel_norms, ffn_reorder  # noqa: F401

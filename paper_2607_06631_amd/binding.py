@@ -94,6 +94,8 @@ def lib():
             "dif_block_forward": (i32, [vp, i32, vp, vp, vp, i32, i32, i32, vp, sz, vp]),
             "dif_step_forward": (i32, [vp, vp, f32, vp, i32, i32, i32, vp, vp, sz, vp]),
             "dif_euler": (i32, [vp, vp, f32, f32, i64, vp]),
+            "dif_hard_gates": (i32, [C.POINTER(DifConfig), i32] + [vp] * 8),
+            "dif_ffn_reorder": (i32, [vp, i32, vp, vp, vp, vp, vp, sz, vp]),
             "dif_renoise": (i32, [vp, vp, f32, f32, vp, i64, vp]),
             "dif_rollout": (i32, [C.POINTER(vp), C.POINTER(f32), i32, i32, vp, C.POINTER(vp), vp,
                                   i32, i32, i32, vp, vp, sz, vp]),
@@ -297,6 +299,38 @@ def dif_step_forward(plan: Plan, z, t: float, ctx, v_out, ws, stream=None) -> No
     Lc = ctx.shape[1]
     _check(lib().dif_step_forward(plan.handle, _ptr(z), float(t), _ptr(ctx), B, L, Lc, _ptr(v_out),
                                   _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def dif_hard_gates(cfg, m_block, m_self, m_cross, m_ffn, chunk: int = 8):
+    """Keep masks of one step from its continuous masks (host arrays)."""
+    import numpy as np
+    N, H, F = cfg.n_layers, cfg.n_heads, cfg.ffn_dim
+    c = make_config(cfg)
+    ins = [np.ascontiguousarray(a, dtype=np.float32) for a in (m_block, m_self, m_cross, m_ffn)]
+    out = {"block_keep": np.zeros(N, np.uint8), "self_head_keep": np.zeros((N, H), np.uint8),
+           "cross_head_keep": np.zeros((N, H), np.uint8), "ffn_keep": np.zeros((N, F), np.uint8)}
+    ptrs = [a.ctypes.data for a in ins] + [out[k].ctypes.data for k in
+                                           ("block_keep", "self_head_keep", "cross_head_keep", "ffn_keep")]
+    _check(lib().dif_hard_gates(C.byref(c), int(chunk), *ptrs))
+    return out
+
+
+def dif_ffn_reorder(model: "Model", layer: int, stream=None):
+    """(perm, w1, b1, w2): the layer's FFN weights with hidden channels sorted
+    by decreasing norm, as new device tensors."""
+    import numpy as np
+    import torch
+    cfg = model.cfg
+    D, F = cfg.dim, cfg.ffn_dim
+    mdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    w1 = torch.empty((F, D), dtype=mdt, device="cuda")
+    w2 = torch.empty((D, F), dtype=mdt, device="cuda")
+    b1 = torch.empty((F,), dtype=torch.float32, device="cuda")
+    scratch = torch.empty(F * 12 + 16, dtype=torch.uint8, device="cuda")
+    perm = np.zeros(F, np.int32)
+    _check(lib().dif_ffn_reorder(model.handle, layer, _ptr(w1), _ptr(b1), _ptr(w2),
+                                 perm.ctypes.data, _ptr(scratch), scratch.numel(), _stream(stream)))
+    return perm, w1, b1, w2
 
 
 DIF_SAMPLER_EULER, DIF_SAMPLER_RENOISE = 0, 1

@@ -960,6 +960,82 @@ dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int
   GUARD_END
 }
 
+dif_status dif_hard_gates(const dif_config* cfg, int32_t chunk, const float* m_block,
+                          const float* m_self, const float* m_cross, const float* m_ffn,
+                          uint8_t* block_keep, uint8_t* self_head_keep, uint8_t* cross_head_keep,
+                          uint8_t* ffn_keep) {
+  GUARD_BEGIN
+  DIF_TRY(check_config(cfg));
+  if (!m_block || !m_self || !m_cross || !m_ffn || !block_keep || !self_head_keep ||
+      !cross_head_keep || !ffn_keep)
+    return fail(DIF_E_ARG, "null argument");
+  const int N = cfg->n_layers, H = cfg->n_heads, dh = cfg->head_dim, F = cfg->ffn_dim;
+  if (chunk < 1 || F % chunk != 0)
+    return fail(DIF_E_SHAPE, "ffn_dim %d is not a multiple of the chunk %d", F, chunk);
+  const int nc = F / chunk;
+  for (int l = 0; l < N; ++l) {
+    block_keep[l] = m_block[l] > 0.f ? 1 : 0;
+    const float* ms[2] = {m_self + (size_t)l * H * dh, m_cross + (size_t)l * H * dh};
+    uint8_t* ks[2] = {self_head_keep + (size_t)l * H, cross_head_keep + (size_t)l * H};
+    for (int a = 0; a < 2; ++a)
+      for (int h = 0; h < H; ++h) {
+        double sum = 0.0;   // mean > 0  <=>  sum > 0
+        for (int d = 0; d < dh; ++d) sum += (double)ms[a][h * dh + d];
+        ks[a][h] = sum > 0.0 ? 1 : 0;
+      }
+    for (int c = 0; c < nc; ++c) {
+      const uint8_t g = m_ffn[(size_t)l * nc + c] > 0.f ? 1 : 0;
+      std::memset(ffn_keep + (size_t)l * F + (size_t)c * chunk, g, chunk);
+    }
+  }
+  return DIF_OK;
+  GUARD_END
+}
+
+dif_status dif_ffn_reorder(const dif_model* model, int32_t layer, void* w1_out, float* b1_out,
+                           void* w2_out, int32_t* perm_out, void* scratch, size_t scratch_bytes,
+                           dif_stream stream) {
+  GUARD_BEGIN
+  if (!model || !w1_out || !b1_out || !w2_out || !perm_out || !scratch)
+    return fail(DIF_E_ARG, "null argument");
+  const dif_config& c = model->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(DIF_E_ARG, "layer %d out of range", layer);
+  const int D = c.dim, F = c.ffn_dim;
+  if (scratch_bytes < (size_t)F * (sizeof(double) + sizeof(int32_t)))
+    return fail(DIF_E_WORKSPACE, "scratch %zu bytes < %zu", scratch_bytes,
+                (size_t)F * (sizeof(double) + sizeof(int32_t)));
+  if (reinterpret_cast<uintptr_t>(scratch) % 8) return fail(DIF_E_WORKSPACE, "scratch not 8-byte aligned");
+  const dif_layer_weights& W = model->layers[layer];
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  double* norms = static_cast<double*>(scratch);
+  int32_t* dperm = reinterpret_cast<int32_t*>(norms + F);
+  if (c.dtype == DIF_BF16)
+    HIP_TRY(dif::launch_ffn_norms<bf16>((const bf16*)W.ffn_w1, W.ffn_b1, (const bf16*)W.ffn_w2, D, F,
+                                        norms, s));
+  else
+    HIP_TRY(dif::launch_ffn_norms<float>((const float*)W.ffn_w1, W.ffn_b1, (const float*)W.ffn_w2, D,
+                                         F, norms, s));
+  std::vector<double> hn(F);
+  HIP_TRY(hipMemcpyAsync(hn.data(), norms, F * sizeof(double), hipMemcpyDeviceToHost, s));
+  HIP_TRY(hipStreamSynchronize(s));
+  std::vector<int32_t> perm(F);
+  for (int j = 0; j < F; ++j) perm[j] = j;
+  std::stable_sort(perm.begin(), perm.end(), [&](int32_t a, int32_t b) { return hn[a] > hn[b]; });
+  std::memcpy(perm_out, perm.data(), F * sizeof(int32_t));
+  HIP_TRY(hipMemcpyAsync(dperm, perm.data(), F * sizeof(int32_t), hipMemcpyHostToDevice, s));
+  if (c.dtype == DIF_BF16) {
+    HIP_TRY(dif::launch_gather<bf16>((const bf16*)W.ffn_w1, D, (bf16*)w1_out, D, F, D, dperm, nullptr, s));
+    HIP_TRY(dif::launch_gather<bf16>((const bf16*)W.ffn_w2, F, (bf16*)w2_out, F, D, F, nullptr, dperm, s));
+  } else {
+    HIP_TRY(dif::launch_gather<float>((const float*)W.ffn_w1, D, (float*)w1_out, D, F, D, dperm, nullptr, s));
+    HIP_TRY(dif::launch_gather<float>((const float*)W.ffn_w2, F, (float*)w2_out, F, D, F, nullptr, dperm, s));
+  }
+  HIP_TRY(dif::launch_gather<float>(W.ffn_b1, 1, b1_out, 1, F, 1, dperm, nullptr, s));
+  HIP_TRY(hipStreamSynchronize(s));   // the host permutation buffer is released on return
+  return DIF_OK;
+  GUARD_END
+}
+
 dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda, const void* B,
                     int64_t ldb, void* C, int64_t ldc, int32_t M, int32_t N, int32_t K,
                     int32_t epilogue, const float* bias, const float* gate0, const float* gate1,

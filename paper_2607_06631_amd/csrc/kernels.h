@@ -86,6 +86,11 @@ hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out
 hipError_t launch_sinusoid(float t, int dim, float* out, hipStream_t stream);
 hipError_t launch_silu(const float* x, float* y, int n, hipStream_t stream);
 hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStream_t stream);
+
+// out[j] = sqrt(|W1[j, :]|^2 + b1[j]^2 + |W2[:, j]|^2) (double), W1 [F, D], W2 [D, F].
+template <typename T>
+hipError_t launch_ffn_norms(const T* w1, const float* b1, const T* w2, int D, int F, double* out,
+                            hipStream_t stream);
 // z = (1 - sigma_to) (z - sigma_from v) + sigma_to eps; eps null means sigma_to = 0.
 hipError_t launch_renoise(float* z, const float* v, float sigma_from, float sigma_to,
                           const float* eps, int64_t n, hipStream_t stream);

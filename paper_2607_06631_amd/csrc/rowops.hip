@@ -275,6 +275,35 @@ hipError_t launch_gather(const T* src, int64_t lds, T* dst, int64_t ldd, int row
 }
 
 // ---------------------------------------------------------------------------
+// FFN channel norms: sqrt(|W1[j, :]|^2 + b1[j]^2 + |W2[:, j]|^2), in double
+// (one-time preprocessing; a thread per channel, W2 reads coalesced over j)
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void ffn_norms_kernel(const T* __restrict__ w1,
+                                                              const float* __restrict__ b1,
+                                                              const T* __restrict__ w2, int D, int F,
+                                                              double* __restrict__ out) {
+  const int j = blockIdx.x * R_THREADS + threadIdx.x;
+  if (j >= F) return;
+  double acc = (double)b1[j] * (double)b1[j];
+  for (int d = 0; d < D; ++d) {
+    const double v = (double)to_f32(w1[(int64_t)j * D + d]);
+    const double u = (double)to_f32(w2[(int64_t)d * F + j]);
+    acc += v * v + u * u;
+  }
+  out[j] = sqrt(acc);
+}
+
+template <typename T>
+hipError_t launch_ffn_norms(const T* w1, const float* b1, const T* w2, int D, int F, double* out,
+                            hipStream_t stream) {
+  if (F <= 0) return hipSuccess;
+  hipLaunchKernelGGL((ffn_norms_kernel<T>), dim3((F + R_THREADS - 1) / R_THREADS), dim3(R_THREADS), 0,
+                     stream, w1, b1, w2, D, F, out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // timestep embedding pieces
 // ---------------------------------------------------------------------------
 template <typename T>
@@ -392,7 +421,9 @@ hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream) 
                                        const int32_t*, const int32_t*, hipStream_t);           \
   template hipError_t launch_gemv<T>(const T*, const float*, const float*, float*, int, int,   \
                                      hipStream_t);                                             \
-  template hipError_t launch_cast<T>(const float*, T*, int64_t, hipStream_t);
+  template hipError_t launch_cast<T>(const float*, T*, int64_t, hipStream_t);                  \
+  template hipError_t launch_ffn_norms<T>(const T*, const float*, const T*, int, int, double*,  \
+                                          hipStream_t);
 INST(float)
 INST(bf16)
 #undef INST
