@@ -231,3 +231,31 @@ def test_wan13b_width_block_sharp_attention():
     err = rel_err(got, ref)
     say(f"  rel err {err:.3e}")
     assert err <= TOL_BF16_SHARP
+
+
+def test_wan14b_width_step_with_block_skips():
+    """A 4-layer stack at Wan-14B widths whose step structure gates off two
+    blocks and keeps a different head / channel subset in every other layer
+    (block gates, Sec. 4.1; per-layer structures, Sec. 6), through
+    dif_step_forward, for both plan kinds."""
+    import torch
+    cfg = MID14.with_(name="mid14x4", n_layers=4, grid=(1, 7, 11), text_len=64)
+    say(f"wan14b-width 4-layer step with block skips L={cfg.seq_len}")
+    w = synth.make_weights(cfg, seed=2)
+    model = make_model(cfg, w)
+    masks = synth.masks_from_counts(cfg.with_(ffn_chunk=8), [40, 24, 30, 36], [28, 40, 20, 32],
+                                    [13824, 8296, 9680, 11056], seed=9, block_keep=[1, 0, 1, 0])
+    z0 = synth.make_latents(cfg, seed=9)
+    ctx = synth.make_context(cfg, seed=9)
+    ref = O.step(z0, 500, ctx, w, masks, cfg)
+    for kind in ("compact", "indexed"):
+        plan = B.dif_plan_step(model, 2, masks, kind=kind)
+        assert [plan.layer_info(l).block_keep for l in range(4)] == [1, 0, 1, 0]
+        z = to_dev(z0, dtype=torch.float32)
+        v = torch.empty_like(z)
+        ws = B.workspace(model, 1, cfg.seq_len, cfg.text_len)
+        B.dif_step_forward(plan, z, 500, to_dev(ctx, cfg), v, ws)
+        torch.cuda.synchronize()
+        err = rel_err(to_np(v), ref)
+        say(f"  {kind}: rel err {err:.3e}")
+        assert err <= TOL["bf16"]
