@@ -119,10 +119,14 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// GELU with the tanh approximation, 0.5 x (1 + tanh(u)), u = sqrt(2/pi)(x +
+// 0.044715 x^3), evaluated as x / (1 + exp(-2u)) (the identity
+// 0.5 (1 + tanh u) = 1 / (1 + e^{-2u})) with the hardware exp2 and
+// reciprocal; saturates correctly (exp2 -> inf gives 0, -> 0 gives x).
 __device__ __forceinline__ float gelu_tanh(float x) {
-  const float c = 0.7978845608028654f;  // sqrt(2/pi)
-  const float u = c * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.f + tanhf(u));
+  constexpr float k = -2.f * 0.7978845608028654f * 1.4426950408889634f;  // -2 sqrt(2/pi) log2(e)
+  const float t = x * fmaf(0.044715f * x, x, 1.f);                        // x + 0.044715 x^3
+  return x * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(k * t));
 }
 
 }  // namespace dif

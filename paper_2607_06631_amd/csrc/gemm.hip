@@ -52,7 +52,32 @@ struct GemmParams {
   const int32_t* rows;   // GA_ROWS
   const int32_t* kch;    // GA_KCH
   int b_rows;            // GA_ROWS: rows of the union B matrix
+  int vec4;              // C rows allow aligned 4-element accesses
 };
+
+// four consecutive output elements: 8-byte (bf16) or 16-byte (f32) accesses
+__device__ __forceinline__ void load4(const bf16* p, float* v) {
+  const bf16x4 x = *reinterpret_cast<const bf16x4*>(p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = (float)x[e];
+}
+__device__ __forceinline__ void load4(const float* p, float* v) {
+  const f32x4 x = *reinterpret_cast<const f32x4*>(p);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) v[e] = x[e];
+}
+__device__ __forceinline__ void store4(bf16* p, const float* v) {
+  bf16x4 x;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = (bf16)v[e];
+  *reinterpret_cast<bf16x4*>(p) = x;
+}
+__device__ __forceinline__ void store4(float* p, const float* v) {
+  f32x4 x;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) x[e] = v[e];
+  *reinterpret_cast<f32x4*>(p) = x;
+}
 
 // WGM x WGN waves; each wave owns TM x TN MFMA 32x32 tiles.
 template <typename T, typename OutT, int EPI, int GA, int WGM, int WGN, int TM, int TN>
@@ -219,38 +244,79 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   if (kt < nk) ktile(kt, ra1, rb1, ra0, rb0);
   __syncthreads();
 
-  // epilogue: lane holds column n of each tile, 16 rows
+  // Epilogue through LDS (the operand buffers are free after the last
+  // barrier).  A lane holds one column of each 32x32 tile, so direct stores
+  // would move two bytes per lane; instead each wave stages its 128 x 64
+  // block in two passes of 64 rows as float32 (bias added, GELU or the
+  // column gate applied) in its own 16 KB of LDS, then moves rows of four
+  // consecutive elements per lane: 16 lanes cover a 64-column row, so loads
+  // of the residual and the stores are whole 128-byte (bf16) row segments.
+  // The staging layout flips column bit 5 every four rows, which keeps both
+  // the column writes and the row reads free of bank conflicts.
+  static_assert(TM * 32 == 128 && TN * 32 == 64, "epilogue staging assumes 128 x 64 per wave");
+  float* stage = reinterpret_cast<float*>(&smem[0][0][0]) + wave * (64 * 64);
+  auto sidx = [](int r, int c) { return r * 64 + (c ^ (((r >> 2) & 1) << 5)); };
+  float colv[TN], gatev[TN];
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int n = n0 + wn * TN * 32 + j * 32 + col;
-    if (n >= p.N) continue;
-    float bias = 0.f;
-    if constexpr (GA == GA_ROWS) {
-      const int r = p.rows[n];
-      if (bias_sg && r >= 0) bias = bias_sg[r];
-    } else {
-      if (bias_sg) bias = bias_sg[n];
+    colv[j] = 0.f;
+    gatev[j] = 1.f;
+    if (n < p.N) {
+      if constexpr (GA == GA_ROWS) {
+        const int r = p.rows[n];
+        if (bias_sg && r >= 0) colv[j] = bias_sg[r];
+      } else {
+        if (bias_sg) colv[j] = bias_sg[n];
+      }
+      if (EPI == EPI_RESIDUAL && p.gate0) gatev[j] = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
     }
-    float gate = 1.f;
-    if (EPI == EPI_RESIDUAL && p.gate0) gate = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
+  }
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+  for (int pass = 0; pass < 2; ++pass) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + wm * TM * 32 + i * 32 + acc_row(r, g);
-        if (m < p.M) {
-          OutT* dst = Csg + (int64_t)m * p.ldc + n;
-          const float v = acc[i][j][r] + bias;
-          if (EPI == EPI_STORE) {
-            *dst = from_f32<OutT>(v);
-          } else if (EPI == EPI_GELU) {
-            *dst = from_f32<OutT>(gelu_tanh(v));
-          } else {
-            *dst = from_f32<OutT>(to_f32(*dst) + gate * v);
-          }
+    for (int ii = 0; ii < 2; ++ii) {
+      const int i = 2 * pass + ii;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          float v = acc[i][j][r] + colv[j];
+          if (EPI == EPI_GELU) v = gelu_tanh(v);
+          if (EPI == EPI_RESIDUAL) v *= gatev[j];
+          stage[sidx(ii * 32 + acc_row(r, g), j * 32 + col)] = v;
         }
+    }
+    __syncthreads();
+    const int cq = lane & 15;                          // 4-column chunk of the row
+    const int nb = n0 + wn * TN * 32 + cq * 4;
+    const bool full4 = p.vec4 && nb + 4 <= p.N;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int rl = t * 4 + (lane >> 4);              // row within the pass
+      const int m = m0 + wm * TM * 32 + pass * 64 + rl;
+      const f32x4 sv = *reinterpret_cast<const f32x4*>(&stage[sidx(rl, cq * 4)]);
+      float v[4] = {sv[0], sv[1], sv[2], sv[3]};
+      if (m >= p.M || nb >= p.N) continue;
+      OutT* dst = Csg + (int64_t)m * p.ldc + nb;
+      if (full4) {
+        if constexpr (EPI == EPI_RESIDUAL) {
+          float xr[4];
+          load4(dst, xr);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += xr[e];
+        }
+        store4(dst, v);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          if (nb + e < p.N) {
+            if (EPI == EPI_RESIDUAL) v[e] += to_f32(dst[e]);
+            dst[e] = from_f32<OutT>(v[e]);
+          }
       }
     }
+    if (pass == 0) __syncthreads();   // reads done before the second pass overwrites
   }
 }
 
@@ -296,6 +362,7 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
   p.nseg = 1;
   p.gate0 = gate0;
   p.gate1 = gate1;
+  p.vec4 = (ldc % 4 == 0) && (reinterpret_cast<uintptr_t>(C) % (4 * sizeof(OutT)) == 0);
   if (gather && gather->nseg > 1) {
     if (gather->nseg > kMaxSeg || epi == EPI_RESIDUAL) return hipErrorInvalidValue;
     p.nseg = gather->nseg;

@@ -71,6 +71,40 @@ def test_gemm_gelu_and_residual_epilogues(dtype):
     assert rel_err(to_np(X), x0 + (g0 + g1) * acc) <= tol
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("ldc_pad", [0, 3])
+def test_gemm_ragged_columns_and_unaligned_rows(dtype, ldc_pad):
+    """N not a multiple of 4 and (ldc_pad = 3) rows that are not 4-element
+    aligned: the epilogue's element-wise path; nothing outside C is written."""
+    import torch
+    say(f"gemm ragged {dtype} ldc_pad={ldc_pad}")
+    g = np.random.default_rng(11 + ldc_pad)
+    bf = dtype == "bf16"
+    tdt = torch.bfloat16 if bf else torch.float32
+    M, N, K = 300, 203, 64
+    ldc = N + ldc_pad
+    a, b = _rand(g, (M, K), 0.5, bf), _rand(g, (N, K), 0.5, bf)
+    bias = g.standard_normal(N).astype(np.float32)
+    g0 = g.standard_normal(N).astype(np.float32)
+    x0 = _rand(g, (M, N), 1.0, bf)
+    A, Bm = torch.from_numpy(a).cuda().to(tdt), torch.from_numpy(b).cuda().to(tdt)
+    acc = a.astype(np.float64) @ b.astype(np.float64).T + bias
+    tol = 8e-3 if bf else 1e-5
+    for epi in (B.EPI_STORE, B.EPI_GELU, B.EPI_RESIDUAL):
+        buf = torch.full((M + 1, ldc), 7.0, device="cuda", dtype=tdt)
+        if epi == B.EPI_RESIDUAL:
+            buf[:M, :N] = torch.from_numpy(x0).cuda().to(tdt)
+        C = buf[:M]
+        B.dif_gemm(A, Bm, C, epi, bias=torch.from_numpy(bias).cuda(),
+                   gate0=torch.from_numpy(g0).cuda() if epi == B.EPI_RESIDUAL else None,
+                   N=N, ldc=ldc)
+        torch.cuda.synchronize()
+        out = to_np(buf)
+        ref = {B.EPI_STORE: acc, B.EPI_GELU: O.gelu_tanh(acc), B.EPI_RESIDUAL: x0 + g0 * acc}[epi]
+        assert rel_err(out[:M, :N], ref) <= tol
+        assert np.all(out[:M, N:] == 7.0) and np.all(out[M] == 7.0)
+
+
 def _attn_case(dtype, dh, H, Lq, Lk, Bn=1, qscale=1.0, seed=0):
     import torch
     g = np.random.default_rng(seed)
