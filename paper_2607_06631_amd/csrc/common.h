@@ -113,10 +113,24 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// Sum over the 64 lanes of a wave, returned to every lane.  DPP steps:
+// pairs and quads (quad_perm), 8 lanes (row_half_mirror), 16 lanes
+// (row_mirror), then row 0 into row 1 and row 2 into row 3 (row_bcast:15,
+// rows 1 and 3 only) and rows 0-1 into rows 2-3 (row_bcast:31, rows 2 and 3
+// only); lane 63 then holds the total, which is read back as a scalar.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float v) {
+  const int t = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROW_MASK, 0xf, false);
+  return v + __builtin_bit_cast(float, t);
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v = dpp_add<0xb1, 0xf>(v);    // quad_perm [1,0,3,2]
+  v = dpp_add<0x4e, 0xf>(v);    // quad_perm [2,3,0,1]
+  v = dpp_add<0x141, 0xf>(v);   // row_half_mirror
+  v = dpp_add<0x140, 0xf>(v);   // row_mirror
+  v = dpp_add<0x142, 0xa>(v);   // row_bcast:15
+  v = dpp_add<0x143, 0xc>(v);   // row_bcast:31
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 63));
 }
 
 // GELU with the tanh approximation, 0.5 x (1 + tanh(u)), u = sqrt(2/pi)(x +
