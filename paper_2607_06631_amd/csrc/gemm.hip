@@ -4,12 +4,13 @@
 // per-lane layout the MFMA operands want: every lane feeds a 16-byte run of
 // consecutive k.  Workgroup tile 256 x 256, k-tile 128 bytes per row (64
 // bf16 / 32 f32), split over a grid of waves that each own a block of
-// MFMA 32x32 tiles.  Operand tiles are staged through LDS, double-buffered
-// (2 x 64 KB of the 160 KB LDS), with the 16-byte chunks of each row
-// XOR-swizzled (swz) so both the row-contiguous stores and the 32-row
-// fragment reads are bank-conflict free.  Global loads (buffer loads on
-// block-local descriptors) run two k-tiles ahead through two register
-// staging sets.  Ragged M and N: rows past the matrix read as zero through
+// MFMA 32x32 tiles.  Operand tiles are copied global -> LDS by buffer loads
+// that write LDS directly (no staging registers, no LDS store
+// instructions), double-buffered (2 x 64 KB of the 160 KB LDS): tile kt+1
+// is requested while tile kt is computed.  The 16-byte chunks of each row
+// are XOR-swizzled (swz) so the 32-row fragment reads are bank-conflict
+// free; each lane fetches the chunk that the swizzle places in the LDS slot
+// its load writes.  Ragged M and N: rows past the matrix read as zero through
 // the descriptor bounds and stores are predicated; K must be a multiple of
 // the k-tile (the plan pads pruned widths to 64).
 //
@@ -130,19 +131,25 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   const __amdgpu_buffer_rsrc_t b_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(b_base), (short)0, b_bytes, kRsrcWord3);
   uint32_t a_off[LA], b_off[LB];
+  // direct-to-LDS: instruction i of this wave fills LDS rows (i*8 + wave)*8
+  // .. +8 (1 KB); lane l writes 16 bytes at 16*l, i.e. row +l/8, physical
+  // chunk l%8, and fetches the logical chunk the swizzle places there.
+  static_assert(NT == 512 && LA == 4 && LB == 4, "direct staging layout");
+  const int dchunk = (lane & 7) ^ (lane >> 3) ^ (wave & 1);   // logical chunk (same for all i)
+  auto drow = [&](int i) { return (i * 8 + wave) * 8 + (lane >> 3); };
 #pragma unroll
   for (int i = 0; i < LA; ++i)
-    a_off[i] = (uint32_t)(((lr + RPL * i) * p.lda + lc * VEC) * (int64_t)sizeof(T));
+    a_off[i] = (uint32_t)((drow(i) * p.lda + dchunk * VEC) * (int64_t)sizeof(T));
 #pragma unroll
   for (int i = 0; i < LB; ++i) {
     if constexpr (GA == GA_ROWS) {
-      const int n = n0 + lr + RPL * i;
+      const int n = n0 + drow(i);
       const int r = n < p.N ? p.rows[n] : -1;
-      b_off[i] = r >= 0 ? (uint32_t)((r * p.ldb + lc * VEC) * (int64_t)sizeof(T)) : kMasked;
+      b_off[i] = r >= 0 ? (uint32_t)((r * p.ldb + dchunk * VEC) * (int64_t)sizeof(T)) : kMasked;
     } else if constexpr (GA == GA_KCH) {
-      b_off[i] = (uint32_t)((lr + RPL * i) * p.ldb * (int64_t)sizeof(T));   // chunk added per k-tile
+      b_off[i] = (uint32_t)(drow(i) * p.ldb * (int64_t)sizeof(T));
     } else {
-      b_off[i] = (uint32_t)(((lr + RPL * i) * p.ldb + lc * VEC) * (int64_t)sizeof(T));
+      b_off[i] = (uint32_t)((drow(i) * p.ldb + dchunk * VEC) * (int64_t)sizeof(T));
     }
   }
   const int nk = p.K / BK;
@@ -154,43 +161,31 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
     __syncthreads();
   }
 
-  // Two register staging sets: tile kt+2 is requested while tile kt is
-  // computed, so global latency is hidden behind two compute phases.
-  u32x4 ra0[LA], rb0[LB], ra1[LA], rb1[LB];
-  // GA_KCH: byte offset of this thread's chunk for the next tile to load,
-  // read from LDS one k-tile ahead so the loads never wait on it
-  uint32_t kb = 0;
+  uint32_t kb = 0;   // GA_KCH: byte offset of this lane's chunk in the next tile to issue
   auto kb_fetch = [&](int kt) {
     if constexpr (GA == GA_KCH) {
-      if (kt < nk) kb = kch_lds[kt * G_CH + lc];
+      if (kt < nk) kb = kch_lds[kt * G_CH + dchunk];
     }
   };
-  auto gload = [&](int kt, u32x4* ra, u32x4* rb) {
+  typedef __attribute__((address_space(3))) void lds_t;
+  auto issue = [&](int kt) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int st = kt & 1;
     const int koff = kt * BK * (int)sizeof(T);
 #pragma unroll
     for (int i = 0; i < LA; ++i)
-      ra[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(a_rsrc, a_off[i], koff, 0));
-    if constexpr (GA == GA_KCH) {
-#pragma unroll
-      for (int i = 0; i < LB; ++i)
-        rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i] + kb, 0, 0));
-    } else {
-#pragma unroll
-      for (int i = 0; i < LB; ++i)
-        rb[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(b_rsrc, b_off[i], koff, 0));
-    }
-  };
-  auto sstore = [&](int buf, const u32x4* ra, const u32x4* rb) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) {
-      const int row = lr + RPL * i;
-      smem[buf][row][swz<G_CH>(row, lc)] = ra[i];
-    }
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, (lds_t*)&smem[st][(i * 8 + wave) * 8][0], 16,
+                                               a_off[i], koff, 0, 0);
 #pragma unroll
     for (int i = 0; i < LB; ++i) {
-      const int row = lr + RPL * i;
-      smem[buf][BM + row][swz<G_CH>(row, lc)] = rb[i];
+      if constexpr (GA == GA_KCH)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, (lds_t*)&smem[st][BM + (i * 8 + wave) * 8][0],
+                                                 16, b_off[i] + kb, 0, 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, (lds_t*)&smem[st][BM + (i * 8 + wave) * 8][0],
+                                                 16, b_off[i], koff, 0, 0);
     }
+#endif
   };
 
   f32x16 acc[TM][TN];
@@ -216,32 +211,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
         for (int j = 0; j < TN; ++j) Mma<T>::step(acc[i][j], af[i], bfr[j]);
     }
   };
-  // one k-tile: after the barrier tile kt is visible and buffer (kt+1)&1 is
-  // free; `cur` holds tile kt+1 (stored first), `nxt` receives tile kt+2
-  auto ktile = [&](int kt, u32x4* ra_cur, u32x4* rb_cur, u32x4* ra_nxt, u32x4* rb_nxt) {
-    __syncthreads();
-    if (kt + 1 < nk) sstore((kt + 1) & 1, ra_cur, rb_cur);
-    if (kt + 2 < nk) {
-      gload(kt + 2, ra_nxt, rb_nxt);
-      kb_fetch(kt + 3);
-    }
-    compute(kt & 1);
-  };
-
+  // one k-tile: wait for this wave's loads of tile kt, barrier (everyone's
+  // have landed and everyone is done with tile kt-1's stage), issue tile
+  // kt+1 into that stage, compute tile kt
   if (nk > 0) {
     kb_fetch(0);
-    gload(0, ra0, rb0);
-    sstore(0, ra0, rb0);
+    issue(0);
     kb_fetch(1);
-    if (nk > 1) gload(1, ra1, rb1);
-    kb_fetch(2);
   }
-  int kt = 0;
-  for (; kt + 1 < nk; kt += 2) {
-    ktile(kt, ra1, rb1, ra0, rb0);       // tile kt+1 is in set 1, kt+2 goes to set 0
-    ktile(kt + 1, ra0, rb0, ra1, rb1);   // tile kt+2 is in set 0, kt+3 goes to set 1
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_vmcnt<0>();
+    __syncthreads();
+    if (kt + 1 < nk) {
+      issue(kt + 1);
+      kb_fetch(kt + 2);
+    }
+    compute(kt & 1);
   }
-  if (kt < nk) ktile(kt, ra1, rb1, ra0, rb0);
   __syncthreads();
 
   // Epilogue through LDS (the operand buffers are free after the last
@@ -320,22 +306,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   }
 }
 
-// Tile shapes: 256 x 256 workgroup tile as 8 waves of 128 x 64 (default)
-// or 4 waves of 128 x 128.
-#ifndef DIF_GEMM_WAVES
-#define DIF_GEMM_WAVES 8
-#endif
-
 // LDS left beside the two 64 KB operand buffers for the K-chunk table
 constexpr int kMaxKChunks = (160 * 1024 - 2 * 64 * 1024) / 4;
 
+// 256 x 256 workgroup tile as 8 waves (2 x 4) of 128 x 64.
 template <typename T, typename OutT, int EPI, int GA>
 void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
-#if DIF_GEMM_WAVES == 4
-  constexpr int WGM = 2, WGN = 2, TM = 4, TN = 4;
-#else
   constexpr int WGM = 2, WGN = 4, TM = 4, TN = 2;
-#endif
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.nseg;
   const size_t dyn = GA == GA_KCH ? (size_t)(p.K / Chunk<T>::VEC) * sizeof(uint32_t) : 0;
