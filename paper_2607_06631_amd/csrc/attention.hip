@@ -243,6 +243,9 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
     for (int kk = 0; kk < 2; ++kk) {
       __builtin_amdgcn_sched_barrier(0);   // halves are not interleaved (register budget)
       f32x16 s = scores(buf, kk, negm);   // (scores - m) in MFMA output units
+      // (the tail tile masks before its V^T reads: fewer registers live
+      // across the branch)
+      if (MASKED && key0 + kk * 32 + 32 > p.Lk) mask(s, key0 + kk * 32);
       // V^T fragments of this half, in flight during the softmax
       u32x4 vf[NPC][DH / 32];
 #pragma unroll
@@ -251,7 +254,6 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
         for (int dt = 0; dt < DH / 32; ++dt)
           vf[u][dt] = vs_[buf][dt * 32 + col][swz<VCH>(col, (kk * 32 + 16 * g) / VEC + u)];
       __builtin_amdgcn_sched_barrier(0);
-      if (MASKED && key0 + kk * 32 + 32 > p.Lk) mask(s, key0 + kk * 32);
       if constexpr (!SC) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[r] *= uscale;
@@ -288,8 +290,15 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
 #pragma unroll
         for (int e = 0; e < VEC; ++e) pv[e] = __builtin_amdgcn_exp2f(s[u * VEC + e]);
         pc[u] = Chunk<T>::pack(pv);
+        // pairwise sum of the chunk (short dependency chains), then into l
+        float t[VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) l_run += pv[e];
+        for (int e = 0; e < VEC; ++e) t[e] = pv[e];
+#pragma unroll
+        for (int w = VEC / 2; w > 0; w /= 2)
+#pragma unroll
+          for (int e = 0; e < w; ++e) t[e] += t[e + w];
+        l_run += t[0];
       }
 #pragma unroll
       for (int u = 0; u < NPC; ++u)
