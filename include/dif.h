@@ -224,6 +224,42 @@ dif_status dif_step_forward(const dif_plan* plan, const float* z, float t, const
                             int32_t B, int32_t L, int32_t Lc, float* v_out,
                             void* ws, size_t ws_bytes, dif_stream stream);
 
+/* Cross-attention text cache.  The text keys and values of every layer
+ * depend on the context and the layer only, not on the timestep or the
+ * step's structure (Sec. 3.2 routes by step; the context is fixed over the
+ * few-step chain of Sec. 4.2), so they can be projected once per context
+ * for all heads and shared by the steps of a rollout.  Each step then takes
+ * its kept heads from the cache and applies its key RMSNorm (over all D
+ * channels, pruned ones counting as zero, as without the cache), with
+ * results identical to the calls that take ctx.
+ *
+ * dif_text_cache_bytes: device bytes of the cache for B samples of Lc text
+ * tokens (per layer B*Lc*D keys and B*D*round_up(Lc, 64) transposed values
+ * in the model dtype, plus one B*Lc*D staging buffer).
+ * dif_text_cache_build: fills `cache` (caller-owned device memory, 256-byte
+ * aligned, cache_bytes >= the size above) from ctx [B, Lc, D] (dtype),
+ * enqueued on `stream`; 4*B*Lc*D*D*n_layers flops.  The cache stays valid
+ * while the model's weights and the context are unchanged.
+ * Errors: DIF_E_ARG (null model / ctx / cache, misaligned cache),
+ * DIF_E_SHAPE (B < 1, Lc outside [1, max_text_len]), DIF_E_WORKSPACE (cache
+ * too small), DIF_E_HIP. */
+dif_status dif_text_cache_bytes(const dif_model* model, int32_t B, int32_t Lc, size_t* bytes);
+dif_status dif_text_cache_build(const dif_model* model, const void* ctx, int32_t B, int32_t Lc,
+                                void* cache, size_t cache_bytes, dif_stream stream);
+
+/* dif_block_forward / dif_step_forward reading the text keys and values from
+ * a cache built for the same model, B and Lc (which the library cannot check:
+ * a cache of another model or context gives that model's / context's
+ * result).  Same results, bit for bit, as the calls with that context.
+ * Errors: those of the calls with a context, and DIF_E_ARG / DIF_E_WORKSPACE
+ * for a null, misaligned or too small cache. */
+dif_status dif_block_forward_cached(const dif_plan* plan, int32_t layer, void* x, const void* cache,
+                                    size_t cache_bytes, const float* e0, int32_t B, int32_t L,
+                                    int32_t Lc, void* ws, size_t ws_bytes, dif_stream stream);
+dif_status dif_step_forward_cached(const dif_plan* plan, const float* z, float t, const void* cache,
+                                   size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                                   float* v_out, void* ws, size_t ws_bytes, dif_stream stream);
+
 /* Euler update between sampler steps, in place: z += (sigma_to - sigma_from) * v,
  * n float32 elements. */
 dif_status dif_euler(float* z, const float* v, float sigma_from, float sigma_to, int64_t n,
@@ -260,6 +296,15 @@ dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int
                        int32_t sampler, float* z, const float* const* eps, const void* ctx,
                        int32_t B, int32_t L, int32_t Lc, float* v_scratch, void* ws,
                        size_t ws_bytes, dif_stream stream);
+
+/* dif_rollout with the text keys and values read from a cache built by
+ * dif_text_cache_build for the same model, B and Lc: every step shares the
+ * one projection of the context.  Errors: those of dif_rollout and of
+ * dif_step_forward_cached. */
+dif_status dif_rollout_cached(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
+                              int32_t sampler, float* z, const float* const* eps, const void* cache,
+                              size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                              float* v_scratch, void* ws, size_t ws_bytes, dif_stream stream);
 
 /* Hard gates of one step from its continuous masks (Sec. 4.1): block gate
  * 1 iff m_block[l] > 0; a head is kept iff the mean of its head_dim mask

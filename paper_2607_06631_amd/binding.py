@@ -93,12 +93,18 @@ def lib():
             "dif_time_embed": (i32, [vp, f32, vp, vp, vp, sz, vp]),
             "dif_block_forward": (i32, [vp, i32, vp, vp, vp, i32, i32, i32, vp, sz, vp]),
             "dif_step_forward": (i32, [vp, vp, f32, vp, i32, i32, i32, vp, vp, sz, vp]),
+            "dif_block_forward_cached": (i32, [vp, i32, vp, vp, sz, vp, i32, i32, i32, vp, sz, vp]),
+            "dif_step_forward_cached": (i32, [vp, vp, f32, vp, sz, i32, i32, i32, vp, vp, sz, vp]),
+            "dif_text_cache_bytes": (i32, [vp, i32, i32, C.POINTER(sz)]),
+            "dif_text_cache_build": (i32, [vp, vp, i32, i32, vp, sz, vp]),
             "dif_euler": (i32, [vp, vp, f32, f32, i64, vp]),
             "dif_hard_gates": (i32, [C.POINTER(DifConfig), i32] + [vp] * 8),
             "dif_ffn_reorder": (i32, [vp, i32, vp, vp, vp, vp, vp, sz, vp]),
             "dif_renoise": (i32, [vp, vp, f32, f32, vp, i64, vp]),
             "dif_rollout": (i32, [C.POINTER(vp), C.POINTER(f32), i32, i32, vp, C.POINTER(vp), vp,
                                   i32, i32, i32, vp, vp, sz, vp]),
+            "dif_rollout_cached": (i32, [C.POINTER(vp), C.POINTER(f32), i32, i32, vp, C.POINTER(vp),
+                                         vp, sz, i32, i32, i32, vp, vp, sz, vp]),
             "dif_gemm": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp, vp, vp, vp]),
             "dif_attention": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp]),
             "dif_profile_enable": (i32, [i32]),
@@ -301,6 +307,43 @@ def dif_step_forward(plan: Plan, z, t: float, ctx, v_out, ws, stream=None) -> No
                                   _ptr(ws), ws.numel(), _stream(stream)))
 
 
+class TextCache:
+    """Device memory holding every layer's text keys and values for one
+    context (B samples of Lc tokens); built by dif_text_cache_build."""
+
+    def __init__(self, mem, B: int, Lc: int):
+        self.mem, self.B, self.Lc = mem, B, Lc
+
+
+def dif_text_cache_bytes(model: Model, B: int, Lc: int) -> int:
+    n = C.c_size_t()
+    _check(lib().dif_text_cache_bytes(model.handle, B, Lc, C.byref(n)))
+    return n.value
+
+
+def dif_text_cache_build(model: Model, ctx, stream=None) -> TextCache:
+    import torch
+    B, Lc = ctx.shape[0], ctx.shape[1]
+    mem = torch.empty(dif_text_cache_bytes(model, B, Lc), dtype=torch.uint8, device=ctx.device)
+    _check(lib().dif_text_cache_build(model.handle, _ptr(ctx), B, Lc, _ptr(mem), mem.numel(),
+                                      _stream(stream)))
+    return TextCache(mem, B, Lc)
+
+
+def dif_block_forward_cached(plan: Plan, layer: int, x, cache: TextCache, e0, ws, stream=None) -> None:
+    B, L = x.shape[0], x.shape[1]
+    _check(lib().dif_block_forward_cached(plan.handle, layer, _ptr(x), _ptr(cache.mem),
+                                          cache.mem.numel(), _ptr(e0), B, L, cache.Lc, _ptr(ws),
+                                          ws.numel(), _stream(stream)))
+
+
+def dif_step_forward_cached(plan: Plan, z, t: float, cache: TextCache, v_out, ws, stream=None) -> None:
+    B, L = z.shape[0], z.shape[1]
+    _check(lib().dif_step_forward_cached(plan.handle, _ptr(z), float(t), _ptr(cache.mem),
+                                         cache.mem.numel(), B, L, cache.Lc, _ptr(v_out), _ptr(ws),
+                                         ws.numel(), _stream(stream)))
+
+
 def dif_hard_gates(cfg, m_block, m_self, m_cross, m_ffn, chunk: int = 8):
     """Keep masks of one step from its continuous masks (host arrays)."""
     import numpy as np
@@ -354,6 +397,21 @@ def dif_rollout(plans, timesteps, z, ctx, v_scratch, ws, eps=None, sampler: str 
     B, L = z.shape[0], z.shape[1]
     _check(lib().dif_rollout(P, ts, n, SAMPLERS[sampler], _ptr(z), E, _ptr(ctx), B, L, ctx.shape[1],
                              _ptr(v_scratch), _ptr(ws), ws.numel(), _stream(stream)))
+
+
+def dif_rollout_cached(plans, timesteps, z, cache: TextCache, v_scratch, ws, eps=None,
+                       sampler: str = "renoise", stream=None) -> None:
+    """dif_rollout with the text keys and values read from `cache`."""
+    n = len(plans)
+    P = (C.c_void_p * n)(*[p.handle for p in plans])
+    ts = (C.c_float * n)(*[float(t) for t in timesteps])
+    E = None
+    if eps is not None:
+        E = (C.c_void_p * n)(*[(_ptr(e) if e is not None else None) for e in eps])
+    B, L = z.shape[0], z.shape[1]
+    _check(lib().dif_rollout_cached(P, ts, n, SAMPLERS[sampler], _ptr(z), E, _ptr(cache.mem),
+                                    cache.mem.numel(), B, L, cache.Lc, _ptr(v_scratch), _ptr(ws),
+                                    ws.numel(), _stream(stream)))
 
 
 def dif_euler(z, v, sigma_from: float, sigma_to: float, stream=None) -> None:

@@ -396,6 +396,43 @@ WsLayout ws_layout(const dif_config& c, int B, int L, int Lc) {
   return w;
 }
 
+// Cross-attention text cache: per layer, the text tokens' keys before their
+// RMSNorm, k = ctx W_ck^T + b_ck [B*Lc, D], and values transposed,
+// v^T [B, D, ldcvt] (zero past Lc), for all heads; then one [B*Lc, D]
+// staging buffer used while building.
+struct TextLayout {
+  size_t k_bytes, vt_bytes, per_layer, stage, total;
+  int64_t ldcvt;
+  size_t k(int l) const { return (size_t)l * per_layer; }
+  size_t vt(int l) const { return (size_t)l * per_layer + k_bytes; }
+};
+
+TextLayout text_layout(const dif_config& c, int B, int Lc) {
+  const size_t es = esize(c.dtype), Mc = (size_t)B * Lc, D = c.dim;
+  TextLayout t{};
+  t.ldcvt = round_up(Lc, 64);
+  t.k_bytes = align256(Mc * D * es);
+  t.vt_bytes = align256((size_t)B * D * t.ldcvt * es);
+  t.per_layer = t.k_bytes + t.vt_bytes;
+  t.stage = (size_t)c.n_layers * t.per_layer;
+  t.total = t.stage + align256(Mc * D * es);
+  return t;
+}
+
+dif_status check_text(const dif_config& c, int B, int Lc) {
+  if (B <= 0) return fail(DIF_E_SHAPE, "B must be >= 1");
+  if (Lc < 1 || Lc > c.max_text_len) return fail(DIF_E_SHAPE, "Lc = %d outside [1, %d]", Lc, c.max_text_len);
+  if ((int64_t)B * Lc * c.dim > ((int64_t)1 << 31) / 2) return fail(DIF_E_SHAPE, "B * Lc too large");
+  return DIF_OK;
+}
+
+dif_status check_cache(const TextLayout& t, const void* cache, size_t bytes) {
+  if (!cache) return fail(DIF_E_ARG, "text cache is null");
+  if (reinterpret_cast<uintptr_t>(cache) % 256) return fail(DIF_E_ARG, "text cache not 256-byte aligned");
+  if (bytes < t.total) return fail(DIF_E_WORKSPACE, "text cache %zu bytes < required %zu", bytes, t.total);
+  return DIF_OK;
+}
+
 dif_status check_ws(const WsLayout& w, const void* ws, size_t bytes) {
   if (!ws) return fail(DIF_E_WORKSPACE, "workspace is null");
   if (reinterpret_cast<uintptr_t>(ws) % 256) return fail(DIF_E_WORKSPACE, "workspace not 256-byte aligned");
@@ -483,7 +520,8 @@ dif_status gather_layer(const dif_model* m, int l, const LayerPlan& lp, hipStrea
 // ---------------------------------------------------------------------------
 template <typename T>
 dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const float* e0, int B,
-                      int L, int Lc, char* ws, const WsLayout& wl, hipStream_t s) {
+                      int L, int Lc, char* ws, const WsLayout& wl, hipStream_t s,
+                      const T* tk = nullptr, const T* tvt = nullptr) {
   const dif_model* m = plan->model;
   const dif_config& c = m->cfg;
   const LayerPlan& lp = plan->lay.layers[layer];
@@ -564,9 +602,23 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
   }
   if (ac > 0) {
     T* cq = big;
-    if (ix) {
+    // With a text cache the step's K / V are the kept heads of the cached
+    // all-head projections (the same values the projection below computes:
+    // each output element's reduction is independent of which rows are kept).
+    const bool cached = tk != nullptr;
+    const int ldk = cached ? ac : 2 * ac;
+    if (ix)
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, (const T*)W.cross_wq, D, cq, ac, M, ac, D,
                           dif::EPI_STORE, W.cross_bq, nullptr, nullptr, s, &g_cross_rows)));
+    else
+      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, lp.at<T>(lp.o_wcq), D, cq, ac, M, ac, D,
+                          dif::EPI_STORE, lp.at<float>(lp.o_bcq), nullptr, nullptr, s)));
+    if (cached) {
+      ProfScope ps(PK_GATHER, s, 0, 4.0 * Mc * ac * es);
+      HIP_TRY(dif::launch_gather_cols16<T>(tk, D, ckv, ldk, Mc, ac, rc, s));
+      HIP_TRY(dif::launch_gather_rows16<T>(tvt, (int64_t)D * wl.ldcvt, cvt, (int64_t)ac * wl.ldcvt,
+                                           wl.ldcvt, ac, B, rc, s));
+    } else if (ix) {
       dif::GemmGather g = g_cross_rows;
       g.nseg = 2;
       g.seg_b[0] = W.cross_wv;
@@ -574,8 +626,6 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wk, D, ckv, 2 * ac, Mc, ac, D,
                           dif::EPI_STORE, W.cross_bk, nullptr, nullptr, s, &g)));
     } else {
-      DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_Q, xn, D, lp.at<T>(lp.o_wcq), D, cq, ac, M, ac, D,
-                          dif::EPI_STORE, lp.at<float>(lp.o_bcq), nullptr, nullptr, s)));
       DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, lp.at<T>(lp.o_wckv), D, ckv, 2 * ac, Mc, 2 * ac, D,
                           dif::EPI_STORE, lp.at<float>(lp.o_bckv), nullptr, nullptr, s)));
     }
@@ -583,15 +633,15 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       ProfScope ps(PK_QK_NORM, s, 0, 2.0 * (M + Mc) * ac * es);
       HIP_TRY(dif::launch_qk_norm<T>(cq, ac, M, ac, 1, 0, 0, ix ? W.cross_gq : lp.at<float>(lp.o_gcq),
                                      nullptr, inv_d, c.eps, nullptr, s, ix ? rc : nullptr, q_scale));
-      HIP_TRY(dif::launch_qk_norm<T>(ckv, 2 * ac, Mc, ac, 1, 0, 0,
+      HIP_TRY(dif::launch_qk_norm<T>(ckv, ldk, Mc, ac, 1, 0, 0,
                                      ix ? W.cross_gk : lp.at<float>(lp.o_gck), nullptr, inv_d, c.eps,
                                      nullptr, s, ix ? rc : nullptr));
     }
-    {
+    if (!cached) {
       ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * Mc * ac * es);
       HIP_TRY(dif::launch_transpose_vt<T>(ckv + ac, 2 * ac, ac, B, Lc, cvt, wl.ldcvt, s));
     }
-    DIF_TRY(attention<T>(PK_ATTN_CROSS, dh, cq, ac, ckv, 2 * ac, cvt, wl.ldcvt, o, ac, B, L, Lc,
+    DIF_TRY(attention<T>(PK_ATTN_CROSS, dh, cq, ac, ckv, ldk, cvt, wl.ldcvt, o, ac, B, L, Lc,
                          lp.info.cross_heads, s, true));
   }
   if (ix)
@@ -642,9 +692,31 @@ dif_status time_embed_impl(const dif_model* m, float t, float* e, float* e0, cha
   return DIF_OK;
 }
 
+// All layers' text projections for context ctx [B, Lc, D].
+template <typename T>
+dif_status text_cache_impl(const dif_model* m, const T* ctx, int B, int Lc, char* cache,
+                           const TextLayout& tl, hipStream_t s) {
+  const dif_config& c = m->cfg;
+  const int D = c.dim, Mc = B * Lc;
+  T* stage = reinterpret_cast<T*>(cache + tl.stage);
+  for (int l = 0; l < c.n_layers; ++l) {
+    const dif_layer_weights& W = m->layers[l];
+    T* k = reinterpret_cast<T*>(cache + tl.k(l));
+    T* vt = reinterpret_cast<T*>(cache + tl.vt(l));
+    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wk, D, k, D, Mc, D, D,
+                        dif::EPI_STORE, W.cross_bk, nullptr, nullptr, s)));
+    DIF_TRY((gemm<T, T>(PK_GEMM_CROSS_KV, ctx, D, (const T*)W.cross_wv, D, stage, D, Mc, D, D,
+                        dif::EPI_STORE, W.cross_bv, nullptr, nullptr, s)));
+    ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * Mc * D * sizeof(T));
+    HIP_TRY(dif::launch_transpose_vt<T>(stage, D, D, B, Lc, vt, tl.ldcvt, s));
+  }
+  return DIF_OK;
+}
+
 template <typename T>
 dif_status step_impl(const dif_plan* plan, const float* z, float t, const T* ctx, int B, int L,
-                     int Lc, float* v, char* ws, const WsLayout& wl, hipStream_t s) {
+                     int Lc, float* v, char* ws, const WsLayout& wl, hipStream_t s,
+                     const char* cache = nullptr, const TextLayout* tl = nullptr) {
   const dif_model* m = plan->model;
   const dif_config& c = m->cfg;
   const int D = c.dim, Cp = c.patch_dim, M = B * L;
@@ -664,7 +736,11 @@ dif_status step_impl(const dif_plan* plan, const float* z, float t, const T* ctx
   }
   DIF_TRY((gemm<T, T>(PK_GEMM_IO, zin, Cp, (const T*)m->w.patch_w, Cp, x, D, M, D, Cp,
                       dif::EPI_STORE, m->w.patch_b, nullptr, nullptr, s)));
-  for (int l = 0; l < c.n_layers; ++l) DIF_TRY(block_impl<T>(plan, l, x, ctx, e0, B, L, Lc, ws, wl, s));
+  for (int l = 0; l < c.n_layers; ++l) {
+    const T* tk = cache ? reinterpret_cast<const T*>(cache + tl->k(l)) : nullptr;
+    const T* tvt = cache ? reinterpret_cast<const T*>(cache + tl->vt(l)) : nullptr;
+    DIF_TRY(block_impl<T>(plan, l, x, ctx, e0, B, L, Lc, ws, wl, s, tk, tvt));
+  }
   {
     ProfScope ps(PK_NORM, s, 0, 2.0 * M * D * sizeof(T));
     HIP_TRY(dif::launch_norm<T>(x, xn, M, D, 0, m->w.head_mod, e, m->w.head_mod + D, e, c.eps, s));
@@ -692,6 +768,83 @@ bool is_gfx950() {
   hipDeviceProp_t prop;
   if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return false;
   return std::strncmp(prop.gcnArchName, "gfx950", 6) == 0;
+}
+
+}  // namespace
+
+namespace {
+
+// Shared by the calls with a context (cache == null) and with a text cache
+// (ctx unused).
+dif_status block_call(const dif_plan* plan, int32_t layer, void* x, const void* ctx,
+                      const void* cache, size_t cache_bytes, const float* e0, int32_t B, int32_t L,
+                      int32_t Lc, void* ws, size_t ws_bytes, dif_stream stream) {
+  DIF_TRY(check_run(plan, B, L, Lc));
+  const dif_config& c = plan->model->cfg;
+  if (layer < 0 || layer >= c.n_layers) return fail(DIF_E_ARG, "layer %d out of range", layer);
+  if (!x || (!ctx && !cache) || !e0) return fail(DIF_E_ARG, "null tensor argument");
+  const TextLayout tl = text_layout(c, B, Lc);
+  if (cache) DIF_TRY(check_cache(tl, cache, cache_bytes));
+  const WsLayout wl = ws_layout(c, B, L, Lc);
+  DIF_TRY(check_ws(wl, ws, ws_bytes));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const char* cb = static_cast<const char*>(cache);
+  if (c.dtype == DIF_BF16)
+    return block_impl<bf16>(plan, layer, (bf16*)x, (const bf16*)ctx, e0, B, L, Lc, w, wl, s,
+                            cb ? (const bf16*)(cb + tl.k(layer)) : nullptr,
+                            cb ? (const bf16*)(cb + tl.vt(layer)) : nullptr);
+  return block_impl<float>(plan, layer, (float*)x, (const float*)ctx, e0, B, L, Lc, w, wl, s,
+                           cb ? (const float*)(cb + tl.k(layer)) : nullptr,
+                           cb ? (const float*)(cb + tl.vt(layer)) : nullptr);
+}
+
+dif_status step_call(const dif_plan* plan, const float* z, float t, const void* ctx,
+                     const void* cache, size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                     float* v_out, void* ws, size_t ws_bytes, dif_stream stream) {
+  DIF_TRY(check_run(plan, B, L, Lc));
+  const dif_config& c = plan->model->cfg;
+  if (!z || (!ctx && !cache) || !v_out) return fail(DIF_E_ARG, "null tensor argument");
+  if (!std::isfinite(t)) return fail(DIF_E_ARG, "timestep is not finite");
+  const TextLayout tl = text_layout(c, B, Lc);
+  if (cache) DIF_TRY(check_cache(tl, cache, cache_bytes));
+  const WsLayout wl = ws_layout(c, B, L, Lc);
+  DIF_TRY(check_ws(wl, ws, ws_bytes));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  const char* cb = static_cast<const char*>(cache);
+  return c.dtype == DIF_BF16
+             ? step_impl<bf16>(plan, z, t, (const bf16*)ctx, B, L, Lc, v_out, w, wl, s, cb, &tl)
+             : step_impl<float>(plan, z, t, (const float*)ctx, B, L, Lc, v_out, w, wl, s, cb, &tl);
+}
+
+dif_status rollout_call(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
+                        int32_t sampler, float* z, const float* const* eps, const void* ctx,
+                        const void* cache, size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                        float* v_scratch, void* ws, size_t ws_bytes, dif_stream stream) {
+  if (!plans || !timesteps || !z || (!ctx && !cache) || !v_scratch) return fail(DIF_E_ARG, "null argument");
+  if (n_steps < 1) return fail(DIF_E_ARG, "n_steps must be >= 1");
+  if (sampler != DIF_SAMPLER_EULER && sampler != DIF_SAMPLER_RENOISE)
+    return fail(DIF_E_ARG, "unknown sampler %d", sampler);
+  for (int i = 0; i < n_steps; ++i) {
+    if (!plans[i]) return fail(DIF_E_ARG, "plan %d is null", i);
+    if (plans[i]->model != plans[0]->model) return fail(DIF_E_ARG, "plans of different models");
+    if (!std::isfinite(timesteps[i])) return fail(DIF_E_ARG, "timestep %d is not finite", i);
+    if (sampler == DIF_SAMPLER_RENOISE && i + 1 < n_steps && (!eps || !eps[i]))
+      return fail(DIF_E_ARG, "re-noise sampler needs eps[%d]", i);
+  }
+  const int64_t n = (int64_t)B * L * plans[0]->model->cfg.patch_dim;
+  for (int i = 0; i < n_steps; ++i) {
+    DIF_TRY(step_call(plans[i], z, timesteps[i], ctx, cache, cache_bytes, B, L, Lc, v_scratch, ws,
+                      ws_bytes, stream));
+    const float sf = timesteps[i] / 1000.f;
+    const float st = i + 1 < n_steps ? timesteps[i + 1] / 1000.f : 0.f;
+    if (sampler == DIF_SAMPLER_EULER)
+      DIF_TRY(dif_euler(z, v_scratch, sf, st, n, stream));
+    else
+      DIF_TRY(dif_renoise(z, v_scratch, sf, st, i + 1 < n_steps ? eps[i] : nullptr, n, stream));
+  }
+  return DIF_OK;
 }
 
 }  // namespace
@@ -868,20 +1021,22 @@ dif_status dif_time_embed(const dif_model* model, float t, float* e_out, float* 
   GUARD_END
 }
 
+
 dif_status dif_block_forward(const dif_plan* plan, int32_t layer, void* x, const void* ctx,
                              const float* e0, int32_t B, int32_t L, int32_t Lc, void* ws,
                              size_t ws_bytes, dif_stream stream) {
   GUARD_BEGIN
-  DIF_TRY(check_run(plan, B, L, Lc));
-  if (layer < 0 || layer >= plan->model->cfg.n_layers) return fail(DIF_E_ARG, "layer %d out of range", layer);
-  if (!x || !ctx || !e0) return fail(DIF_E_ARG, "null tensor argument");
-  const WsLayout wl = ws_layout(plan->model->cfg, B, L, Lc);
-  DIF_TRY(check_ws(wl, ws, ws_bytes));
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  char* w = static_cast<char*>(ws);
-  return plan->model->cfg.dtype == DIF_BF16
-             ? block_impl<bf16>(plan, layer, (bf16*)x, (const bf16*)ctx, e0, B, L, Lc, w, wl, s)
-             : block_impl<float>(plan, layer, (float*)x, (const float*)ctx, e0, B, L, Lc, w, wl, s);
+  if (!ctx) return fail(DIF_E_ARG, "null tensor argument");
+  return block_call(plan, layer, x, ctx, nullptr, 0, e0, B, L, Lc, ws, ws_bytes, stream);
+  GUARD_END
+}
+
+dif_status dif_block_forward_cached(const dif_plan* plan, int32_t layer, void* x, const void* cache,
+                                    size_t cache_bytes, const float* e0, int32_t B, int32_t L,
+                                    int32_t Lc, void* ws, size_t ws_bytes, dif_stream stream) {
+  GUARD_BEGIN
+  if (!cache) return fail(DIF_E_ARG, "text cache is null");
+  return block_call(plan, layer, x, nullptr, cache, cache_bytes, e0, B, L, Lc, ws, ws_bytes, stream);
   GUARD_END
 }
 
@@ -889,16 +1044,41 @@ dif_status dif_step_forward(const dif_plan* plan, const float* z, float t, const
                             int32_t L, int32_t Lc, float* v_out, void* ws, size_t ws_bytes,
                             dif_stream stream) {
   GUARD_BEGIN
-  DIF_TRY(check_run(plan, B, L, Lc));
-  if (!z || !ctx || !v_out) return fail(DIF_E_ARG, "null tensor argument");
-  if (!std::isfinite(t)) return fail(DIF_E_ARG, "timestep is not finite");
-  const WsLayout wl = ws_layout(plan->model->cfg, B, L, Lc);
-  DIF_TRY(check_ws(wl, ws, ws_bytes));
+  if (!ctx) return fail(DIF_E_ARG, "null tensor argument");
+  return step_call(plan, z, t, ctx, nullptr, 0, B, L, Lc, v_out, ws, ws_bytes, stream);
+  GUARD_END
+}
+
+dif_status dif_step_forward_cached(const dif_plan* plan, const float* z, float t, const void* cache,
+                                   size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                                   float* v_out, void* ws, size_t ws_bytes, dif_stream stream) {
+  GUARD_BEGIN
+  if (!cache) return fail(DIF_E_ARG, "text cache is null");
+  return step_call(plan, z, t, nullptr, cache, cache_bytes, B, L, Lc, v_out, ws, ws_bytes, stream);
+  GUARD_END
+}
+
+dif_status dif_text_cache_bytes(const dif_model* model, int32_t B, int32_t Lc, size_t* bytes) {
+  GUARD_BEGIN
+  if (!model || !bytes) return fail(DIF_E_ARG, "null argument");
+  DIF_TRY(check_text(model->cfg, B, Lc));
+  *bytes = text_layout(model->cfg, B, Lc).total;
+  return DIF_OK;
+  GUARD_END
+}
+
+dif_status dif_text_cache_build(const dif_model* model, const void* ctx, int32_t B, int32_t Lc,
+                                void* cache, size_t cache_bytes, dif_stream stream) {
+  GUARD_BEGIN
+  if (!model || !ctx) return fail(DIF_E_ARG, "null argument");
+  const dif_config& c = model->cfg;
+  DIF_TRY(check_text(c, B, Lc));
+  const TextLayout tl = text_layout(c, B, Lc);
+  DIF_TRY(check_cache(tl, cache, cache_bytes));
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  char* w = static_cast<char*>(ws);
-  return plan->model->cfg.dtype == DIF_BF16
-             ? step_impl<bf16>(plan, z, t, (const bf16*)ctx, B, L, Lc, v_out, w, wl, s)
-             : step_impl<float>(plan, z, t, (const float*)ctx, B, L, Lc, v_out, w, wl, s);
+  char* cb = static_cast<char*>(cache);
+  return c.dtype == DIF_BF16 ? text_cache_impl<bf16>(model, (const bf16*)ctx, B, Lc, cb, tl, s)
+                             : text_cache_impl<float>(model, (const float*)ctx, B, Lc, cb, tl, s);
   GUARD_END
 }
 
@@ -929,34 +1109,26 @@ dif_status dif_renoise(float* z, const float* v, float sigma_from, float sigma_t
   GUARD_END
 }
 
+
 dif_status dif_rollout(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
                        int32_t sampler, float* z, const float* const* eps, const void* ctx,
                        int32_t B, int32_t L, int32_t Lc, float* v_scratch, void* ws,
                        size_t ws_bytes, dif_stream stream) {
   GUARD_BEGIN
-  if (!plans || !timesteps || !z || !ctx || !v_scratch) return fail(DIF_E_ARG, "null argument");
-  if (n_steps < 1) return fail(DIF_E_ARG, "n_steps must be >= 1");
-  if (sampler != DIF_SAMPLER_EULER && sampler != DIF_SAMPLER_RENOISE)
-    return fail(DIF_E_ARG, "unknown sampler %d", sampler);
-  for (int i = 0; i < n_steps; ++i) {
-    if (!plans[i]) return fail(DIF_E_ARG, "plan %d is null", i);
-    if (plans[i]->model != plans[0]->model) return fail(DIF_E_ARG, "plans of different models");
-    if (!std::isfinite(timesteps[i])) return fail(DIF_E_ARG, "timestep %d is not finite", i);
-    if (sampler == DIF_SAMPLER_RENOISE && i + 1 < n_steps && (!eps || !eps[i]))
-      return fail(DIF_E_ARG, "re-noise sampler needs eps[%d]", i);
-  }
-  const int64_t n = (int64_t)B * L * plans[0]->model->cfg.patch_dim;
-  for (int i = 0; i < n_steps; ++i) {
-    DIF_TRY(dif_step_forward(plans[i], z, timesteps[i], ctx, B, L, Lc, v_scratch, ws, ws_bytes,
-                             stream));
-    const float sf = timesteps[i] / 1000.f;
-    const float st = i + 1 < n_steps ? timesteps[i + 1] / 1000.f : 0.f;
-    if (sampler == DIF_SAMPLER_EULER)
-      DIF_TRY(dif_euler(z, v_scratch, sf, st, n, stream));
-    else
-      DIF_TRY(dif_renoise(z, v_scratch, sf, st, i + 1 < n_steps ? eps[i] : nullptr, n, stream));
-  }
-  return DIF_OK;
+  if (!ctx) return fail(DIF_E_ARG, "null argument");
+  return rollout_call(plans, timesteps, n_steps, sampler, z, eps, ctx, nullptr, 0, B, L, Lc,
+                      v_scratch, ws, ws_bytes, stream);
+  GUARD_END
+}
+
+dif_status dif_rollout_cached(const dif_plan* const* plans, const float* timesteps, int32_t n_steps,
+                              int32_t sampler, float* z, const float* const* eps, const void* cache,
+                              size_t cache_bytes, int32_t B, int32_t L, int32_t Lc,
+                              float* v_scratch, void* ws, size_t ws_bytes, dif_stream stream) {
+  GUARD_BEGIN
+  if (!cache) return fail(DIF_E_ARG, "text cache is null");
+  return rollout_call(plans, timesteps, n_steps, sampler, z, eps, nullptr, cache, cache_bytes, B, L,
+                      Lc, v_scratch, ws, ws_bytes, stream);
   GUARD_END
 }
 

@@ -78,6 +78,19 @@ template <typename T>
 hipError_t launch_gather(const T* src, int64_t lds, T* dst, int64_t ldd, int rows, int cols,
                          const int32_t* ridx, const int32_t* cidx, hipStream_t stream);
 
+// 16-byte gathers of whole kept heads (idx groups of 16 / sizeof(T) entries
+// are aligned runs of consecutive channels):
+//   cols: dst[r][j] = src[r][idx[j]]                      r < rows, j < cols
+//   rows: dst[b*dst_bs + r*ld + :] = src[b*src_bs + idx[r]*ld + :]   r < rows, b < batches
+// hipErrorInvalidValue when a width / stride is not a whole number of vectors
+// or a base pointer is not 16-byte aligned.
+template <typename T>
+hipError_t launch_gather_cols16(const T* src, int64_t lds, T* dst, int64_t ldd, int rows, int cols,
+                                const int32_t* idx, hipStream_t stream);
+template <typename T>
+hipError_t launch_gather_rows16(const T* src, int64_t src_bs, T* dst, int64_t dst_bs, int64_t ld,
+                                int rows, int batches, const int32_t* idx, hipStream_t stream);
+
 // out[n] = act_out(sum_k W[n,k] * x[k] + bias[n]); W [N, K] row-major.
 template <typename T>
 hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out, int N, int K,

@@ -353,6 +353,73 @@ hipError_t launch_gather(const T* src, int64_t lds, T* dst, int64_t ldd, int row
 }
 
 // ---------------------------------------------------------------------------
+// Kept heads of the cached text projections, 16 bytes per lane.  A kept head
+// is head_dim consecutive channels starting at a multiple of head_dim, so
+// every aligned group of V = 16 / sizeof(T) table entries is one contiguous,
+// aligned 16-byte vector of the source.
+//   cols: dst[r, j] = src[r, idx[j]]              (r < rows, j < cols)
+//   rows: dst[b, r, :] = src[b, idx[r], :]        (r < rows, n per row)
+// ---------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void gather_cols16_kernel(const T* __restrict__ src,
+                                                                  int64_t lds, T* __restrict__ dst,
+                                                                  int64_t ldd, int64_t total, int nvec,
+                                                                  const int32_t* __restrict__ idx) {
+  constexpr int V = 16 / sizeof(T);
+  const int64_t i = (int64_t)blockIdx.x * R_THREADS + threadIdx.x;
+  if (i >= total) return;
+  const int64_t r = i / nvec;
+  const int q = (int)(i - r * nvec);
+  const int sc = idx[q * V];
+  *reinterpret_cast<u32x4*>(dst + r * ldd + (int64_t)q * V) =
+      *reinterpret_cast<const u32x4*>(src + r * lds + sc);
+}
+
+template <typename T>
+__global__ __launch_bounds__(R_THREADS) void gather_rows16_kernel(const T* __restrict__ src,
+                                                                  int64_t src_bs, T* __restrict__ dst,
+                                                                  int64_t dst_bs, int64_t ld, int rows,
+                                                                  const int32_t* __restrict__ idx) {
+  constexpr int V = 16 / sizeof(T);
+  const int64_t nvec = ld / V;
+  const int64_t i = (int64_t)blockIdx.x * R_THREADS + threadIdx.x;
+  if (i >= (int64_t)rows * nvec) return;
+  const int64_t r = i / nvec, q = i - r * nvec;
+  const int64_t b = blockIdx.y;
+  *reinterpret_cast<u32x4*>(dst + b * dst_bs + r * ld + q * V) =
+      *reinterpret_cast<const u32x4*>(src + b * src_bs + (int64_t)idx[r] * ld + q * V);
+}
+
+template <typename T>
+hipError_t launch_gather_cols16(const T* src, int64_t lds, T* dst, int64_t ldd, int rows, int cols,
+                                const int32_t* idx, hipStream_t stream) {
+  constexpr int V = 16 / sizeof(T);
+  if (rows <= 0 || cols <= 0) return hipSuccess;
+  if (cols % V || lds % V || ldd % V || reinterpret_cast<uintptr_t>(src) % 16 ||
+      reinterpret_cast<uintptr_t>(dst) % 16)
+    return hipErrorInvalidValue;
+  const int64_t total = (int64_t)rows * (cols / V);
+  hipLaunchKernelGGL((gather_cols16_kernel<T>), dim3((unsigned)((total + R_THREADS - 1) / R_THREADS)),
+                     dim3(R_THREADS), 0, stream, src, lds, dst, ldd, total, cols / V, idx);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_gather_rows16(const T* src, int64_t src_bs, T* dst, int64_t dst_bs, int64_t ld,
+                                int rows, int batches, const int32_t* idx, hipStream_t stream) {
+  constexpr int V = 16 / sizeof(T);
+  if (rows <= 0 || batches <= 0 || ld <= 0) return hipSuccess;
+  if (ld % V || src_bs % V || dst_bs % V || reinterpret_cast<uintptr_t>(src) % 16 ||
+      reinterpret_cast<uintptr_t>(dst) % 16)
+    return hipErrorInvalidValue;
+  const int64_t total = (int64_t)rows * (ld / V);
+  hipLaunchKernelGGL((gather_rows16_kernel<T>),
+                     dim3((unsigned)((total + R_THREADS - 1) / R_THREADS), (unsigned)batches),
+                     dim3(R_THREADS), 0, stream, src, src_bs, dst, dst_bs, ld, rows, idx);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
 // FFN channel norms: sqrt(|W1[j, :]|^2 + b1[j]^2 + |W2[:, j]|^2), in double
 // (one-time preprocessing; a thread per channel, W2 reads coalesced over j)
 // ---------------------------------------------------------------------------
@@ -497,6 +564,10 @@ hipError_t launch_cast(const float* src, T* dst, int64_t n, hipStream_t stream) 
                                              hipStream_t);                                     \
   template hipError_t launch_gather<T>(const T*, int64_t, T*, int64_t, int, int,               \
                                        const int32_t*, const int32_t*, hipStream_t);           \
+  template hipError_t launch_gather_cols16<T>(const T*, int64_t, T*, int64_t, int, int,        \
+                                              const int32_t*, hipStream_t);                    \
+  template hipError_t launch_gather_rows16<T>(const T*, int64_t, T*, int64_t, int64_t, int, int,\
+                                              const int32_t*, hipStream_t);                    \
   template hipError_t launch_gemv<T>(const T*, const float*, const float*, float*, int, int,   \
                                      hipStream_t);                                             \
   template hipError_t launch_cast<T>(const float*, T*, int64_t, hipStream_t);                  \
