@@ -33,9 +33,9 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "49064d916eda968e140ff7f5091f1a3d01cc35c44e16a683ecfcf208fded84ba",
-    "fetch_bytes": 2108712.5 * 1024 / 0.5,
-    "write_bytes": 415585.9 * 1024 / 1.0,
+    "sha256": "4b373afe2e37c738141fbbfe01f1d15139077c4b760d631b26f85e92e40d55b7",
+    "fetch_bytes": 1205171.5 * 1024 / 0.5,
+    "write_bytes": 382303.3 * 1024 / 1.0,
 }
 
 

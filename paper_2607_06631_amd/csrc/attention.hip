@@ -23,6 +23,9 @@
 // VALU does no per-score scale or subtraction.  Unscaled queries (the plain
 // operator) take one multiply per score instead.
 // Key tails are masked to -inf; V^T chunks past the last key are zero-filled.
+// The MFMA blocks run at raised wave priority, so when both waves of a SIMD
+// are ready the one issuing MFMAs wins and the other's softmax VALU work
+// fills the gaps (measured +2%).
 // The kernel fits in 256 registers per lane (two waves per SIMD).
 #include <type_traits>
 
@@ -190,6 +193,8 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
   auto scores = [&](int buf, int kk, const f32x16& c0) {
     constexpr int KB = NQS >= 8 ? NQS / 2 : NQS;
     f32x16 s = c0;
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s0 = 0; s0 < NQS; s0 += KB) {
       u32x4 kf[KB];
@@ -198,6 +203,8 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
 #pragma unroll
       for (int st = 0; st < KB; ++st) Mma<T>::step(s, kf[st], qf[s0 + st]);
     }
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_setprio(0);
     return s;
   };
   auto mask = [&](f32x16& s, int key) {   // keys >= Lk -> -inf
@@ -300,10 +307,14 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
           for (int e = 0; e < w; ++e) t[e] += t[e + w];
         l_run += t[0];
       }
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(1);
 #pragma unroll
       for (int u = 0; u < NPC; ++u)
 #pragma unroll
         for (int dt = 0; dt < DH / 32; ++dt) Mma<T>::step(o[dt], vf[u][dt], pc[u]);
+      __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
     }
 
     wait_vmcnt<0>();   // tile kt+1 (direct-to-LDS) has landed for this wave
