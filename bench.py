@@ -28,10 +28,11 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
 
 # HBM bytes per self-attention launch over the four step structures, from
 # rocprofv3 FETCH_SIZE and WRITE_SIZE passes scaled by a 2 GiB device copy
-# (read factor 0.5, write factor 1.0).  Valid only for the kernel sources
-# they were measured on; reported as null once those change.
+# (read factor 0.5, write factor 1.0).  Valid only for the workload and the
+# kernel sources they were measured on; reported as null otherwise.
 ATTN_TRAFFIC = {
     "kernel": "attn_self",
+    "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
     "sha256": "4b373afe2e37c738141fbbfe01f1d15139077c4b760d631b26f85e92e40d55b7",
     "fetch_bytes": 1205171.5 * 1024 / 0.5,
@@ -68,12 +69,13 @@ def parse():
     return ap.parse_args()
 
 
-def measured_traffic(kernel):
+def measured_traffic(kernel, workload):
     """HBM bytes per launch of `kernel` from the committed counter passes, or
-    None when the kernel's sources differ from the ones measured."""
+    None for another workload or when the kernel's sources differ from the
+    ones measured."""
     import hashlib
     t = ATTN_TRAFFIC
-    if kernel != t["kernel"]:
+    if kernel != t["kernel"] or workload != t["workload"]:
         return None
     h = hashlib.sha256()
     for f in t["sources"]:
@@ -275,7 +277,7 @@ def main():
             ach = r["flops"] / r["launches"] / (per_launch_ms * 1e-3) / 1e12
             roofline = {"kernel": dom, "bound": "mfma", "achieved": round(ach, 1), "peak": peak,
                         "unit": "TFLOP/s", "frac": round(ach / peak, 4),
-                        "traffic": measured_traffic(dom), "traffic_unit": "HBM bytes per launch",
+                        "traffic": measured_traffic(dom, args.workload), "traffic_unit": "HBM bytes per launch",
                         "avg_launch_ms": round(per_launch_ms, 4)}
         else:
             ach = r["bytes"] / r["launches"] / (per_launch_ms * 1e-3) / 1e9
