@@ -34,9 +34,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "4b373afe2e37c738141fbbfe01f1d15139077c4b760d631b26f85e92e40d55b7",
-    "fetch_bytes": 1205171.5 * 1024 / 0.5,
-    "write_bytes": 382303.3 * 1024 / 1.0,
+    "sha256": "0d151ab01e5d6347df331574888627d1934903d8fa92ccff9627be0697dd1de5",
+    "fetch_bytes": 1166123.8 * 1024 / 0.500,
+    "write_bytes": 392473.6 * 1024 / 1.000,
 }
 
 

@@ -1,7 +1,9 @@
 // Bidirectional flash attention on MFMA for gfx950.
 //
-// Work split: one workgroup = 4 waves of one (sample, head); a wave owns 32
-// queries and walks all keys in tiles of 64, as two 32-key halves.
+// Work split: one workgroup = 8 waves of one (sample, head); a wave owns 32
+// queries and walks all keys in tiles of 64, as two 32-key halves.  Eight
+// waves share each K / V^T tile copied into LDS, which halves those copies
+// per flop against four waves (measured +4%); one workgroup fills a CU.
 //
 // The scores are computed transposed, S^T = K Q^T, with MFMA 32x32 tiles:
 // the A operand is the K tile (rows = keys, from LDS), the B operand is
@@ -34,8 +36,10 @@
 
 namespace dif {
 
-constexpr int AT_WAVES = 4;
-constexpr int AT_THREADS = 64 * AT_WAVES;
+// waves per workgroup: 8 when the keys are long (bf16), 4 for short key
+// sequences (the text tokens), where eight waves leave too few workgroups and
+// too few key tiles to amortise each workgroup's prologue
+constexpr int kLongKeys = 4096;
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
 
@@ -56,9 +60,11 @@ __device__ __forceinline__ int key_slot(int kappa) {
   return 8 * k + 4 * gq + j;
 }
 
-// SC: queries arrive pre-multiplied by log2(e)/sqrt(dh).
-template <typename T, int DH, bool SC>
-__global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(AttnParams<T> p) {
+// SC: queries arrive pre-multiplied by log2(e)/sqrt(dh); AT_WAVES waves per
+// workgroup (4 or 8: two waves per SIMD either way).
+template <typename T, int DH, bool SC, int AT_WAVES>
+__global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel(AttnParams<T> p) {
+  constexpr int AT_THREADS = 64 * AT_WAVES;
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int KCH = DH * (int)sizeof(T) / 16;     // chunks per K row
   constexpr int VCH = AT_BN * (int)sizeof(T) / 16;  // chunks per V^T row
@@ -358,14 +364,23 @@ __global__ __launch_bounds__(AT_THREADS, 8 / AT_WAVES) void flash_attn_kernel(At
     }
 }
 
-template <typename T, int DH>
-void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
-  constexpr int BMQ = AT_WAVES * 32;
+template <typename T, int DH, int W>
+void launch_w(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
+  constexpr int BMQ = W * 32;
   const int blocks = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
   if (q_scaled)
-    hipLaunchKernelGGL((flash_attn_kernel<T, DH, true>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
+    hipLaunchKernelGGL((flash_attn_kernel<T, DH, true, W>), dim3(blocks), dim3(64 * W), 0, stream, p);
   else
-    hipLaunchKernelGGL((flash_attn_kernel<T, DH, false>), dim3(blocks), dim3(AT_THREADS), 0, stream, p);
+    hipLaunchKernelGGL((flash_attn_kernel<T, DH, false, W>), dim3(blocks), dim3(64 * W), 0, stream, p);
+}
+
+template <typename T, int DH>
+void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
+  // (float32 keeps four waves: its head-128 kernel needs one wave per SIMD)
+  if (sizeof(T) == 2 && p.Lk >= kLongKeys)
+    launch_w<T, DH, 8>(p, q_scaled, stream);
+  else
+    launch_w<T, DH, 4>(p, q_scaled, stream);
 }
 
 template <typename T>

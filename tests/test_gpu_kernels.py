@@ -136,8 +136,11 @@ def test_attention_matches_oracle(dtype, dh, Lq, Lk):
     assert err <= (2e-2 if dtype == "bf16" else 1e-5)
 
 
-def test_attention_long_keys_online_softmax():
-    say("attention bf16 long keys")
-    # sharp scores that keep moving the running max across many key tiles
-    err = _attn_case("bf16", 128, 2, 300, 4099, Bn=1, qscale=4.0, seed=11)
+@pytest.mark.parametrize("dh", [128, 64])
+def test_attention_long_keys_online_softmax(dh):
+    say(f"attention bf16 long keys dh={dh} (eight-wave workgroups)")
+    # sharp scores that keep moving the running max across many key tiles;
+    # Lk >= 4096 takes the eight-wave kernel, Lq = 300 ends in a partial
+    # 256-query block and Lk = 4099 in a 3-key tile
+    err = _attn_case("bf16", dh, 2, 300, 4099, Bn=1, qscale=4.0, seed=11)
     assert err <= 2e-2
