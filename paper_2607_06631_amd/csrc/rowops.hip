@@ -5,6 +5,8 @@
 // once; statistics are fp32 whatever the storage type.
 #include <algorithm>
 
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -134,10 +136,14 @@ hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0
 // the sum of squares of the kept channels is divided by D) + 3D RoPE.
 // Gains are staged in LDS once per workgroup.  Lane l always covers the
 // same head-local pairs (64 * VEC is a multiple of head_dim), so its
-// rotation factors are fetched once per row.
+// rotation factors are fetched once per row.  A wave issues the loads of
+// both segments (q and k) of its row before the first reduction waits on
+// them, with the rotation-table reads in their shadow.
 // ---------------------------------------------------------------------------
-template <typename T, int MAXC>
-__global__ __launch_bounds__(64 * NORM_WAVES) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
+constexpr int QK_WAVES = 8;    // 16 KB of loads in flight per wave; registers for both segments
+constexpr int QK_RPW = 16;
+template <typename T, int MAXC, int NSEG>
+__global__ __launch_bounds__(64 * QK_WAVES) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
                                                             int nseg, int off0, int off1,
                                                             const float* g0, const float* g1,
                                                             const int32_t* gidx, float scale0,
@@ -145,7 +151,7 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void qk_norm_kernel(T* buf, int64_
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int NP = VEC / 2;  // pairs per chunk
   extern __shared__ float gain_lds[];  // [nseg][a]
-  for (int n = threadIdx.x; n < a; n += 64 * NORM_WAVES) {
+  for (int n = threadIdx.x; n < a; n += 64 * QK_WAVES) {
     const int gn = gidx ? gidx[n] : n;
     gain_lds[n] = g0[gn] * scale0;
     if (nseg > 1) gain_lds[a + n] = g1[gn];
@@ -154,9 +160,21 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void qk_norm_kernel(T* buf, int64_
   const int lane = threadIdx.x & 63;
   const int nch = a / VEC;
   const int jb = ((lane * VEC) % rope.head_dim) / 2;  // first head-local pair of this lane
-  for (int rr = 0; rr < NORM_RPW; ++rr) {
-    const int64_t row = (int64_t)blockIdx.x * (NORM_WAVES * NORM_RPW) + (threadIdx.x >> 6) * NORM_RPW + rr;
+  for (int rr = 0; rr < QK_RPW; ++rr) {
+    const int64_t row = (int64_t)blockIdx.x * (QK_WAVES * QK_RPW) + (threadIdx.x >> 6) * QK_RPW + rr;
     if (row >= rows) break;
+    // both segments' loads go out before anything waits on them
+    u32x4 raw[NSEG][MAXC];
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg) {
+      const T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
+#pragma unroll
+      for (int i = 0; i < MAXC; ++i) {
+        const int c = lane + kWave * i;
+        if (c < nch) raw[sg][i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
+      }
+    }
+    // rotation factors of this lane's pairs (table reads overlap the loads)
     float cs[NP], sn[NP];
     if (rope.table) {
       const int n = (int)(row % rope.L);
@@ -176,35 +194,38 @@ __global__ __launch_bounds__(64 * NORM_WAVES) void qk_norm_kernel(T* buf, int64_
         sn[k] = rope.table[2 * idx + 1];
       }
     }
-    for (int sg = 0; sg < nseg; ++sg) {
-      T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
-      const float* gain = gain_lds + sg * a;
-      u32x4 raw[MAXC];
+    float rstd[NSEG];
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg) {
       float ss = 0.f;
 #pragma unroll
       for (int i = 0; i < MAXC; ++i) {
         const int c = lane + kWave * i;
         if (c < nch) {
-          raw[i] = *reinterpret_cast<const u32x4*>(xr + c * VEC);
           float v[VEC];
-          Chunk<T>::unpack(raw[i], v);
+          Chunk<T>::unpack(raw[sg][i], v);
 #pragma unroll
           for (int e = 0; e < VEC; ++e) ss += v[e] * v[e];
         }
       }
-      const float rstd = rsqrtf(wave_sum(ss) * inv_dim + eps);
+      rstd[sg] = rsqrtf(wave_sum(ss) * inv_dim + eps);
+    }
+#pragma unroll
+    for (int sg = 0; sg < NSEG; ++sg) {
+      T* xr = buf + row * ld + (sg == 0 ? off0 : off1);
+      const float* gain = gain_lds + sg * a;
 #pragma unroll
       for (int i = 0; i < MAXC; ++i) {
         const int c = lane + kWave * i;
         if (c < nch) {
           float out[VEC];
-          Chunk<T>::unpack(raw[i], out);
+          Chunk<T>::unpack(raw[sg][i], out);
           const f32x4* g4 = reinterpret_cast<const f32x4*>(gain + c * VEC);
 #pragma unroll
           for (int q = 0; q < VEC / 4; ++q) {
             const f32x4 gg = g4[q];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) out[4 * q + e] *= rstd * gg[e];
+            for (int e = 0; e < 4; ++e) out[4 * q + e] *= rstd[sg] * gg[e];
           }
           if (rope.table) {
 #pragma unroll
@@ -232,19 +253,38 @@ hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off
   if (rd.head_dim <= 0) rd.head_dim = 64;   // no rotation: any width dividing 64 * VEC
   constexpr int VEC = Chunk<T>::VEC;
   if ((64 * VEC) % rd.head_dim != 0) return hipErrorInvalidValue;
-  const dim3 grid((rows + NORM_WAVES * NORM_RPW - 1) / (NORM_WAVES * NORM_RPW));
-  const size_t lds = nseg * a * sizeof(float);
-#define QK_LAUNCH(C)                                                                            \
-  hipLaunchKernelGGL((qk_norm_kernel<T, C>), grid, dim3(64 * NORM_WAVES), lds, stream, buf, ld,   \
-                     rows, a, nseg, off0, off1, g0, g1, gain_idx, scale0, inv_norm_dim, eps, rd)
+  const dim3 grid((rows + QK_WAVES * QK_RPW - 1) / (QK_WAVES * QK_RPW));
+  // q and k in one launch while both fit the registers (up to 8 chunks per
+  // lane), else one launch per segment
+  auto launch = [&](auto c_tag, auto nseg_tag, int off_a, int off_b, const float* ga,
+                    const float* gb, float sa) {
+    constexpr int C = decltype(c_tag)::value, NS = decltype(nseg_tag)::value;
+    hipLaunchKernelGGL((qk_norm_kernel<T, C, NS>), grid, dim3(64 * QK_WAVES), NS * a * sizeof(float),
+                       stream, buf, ld, rows, a, NS, off_a, off_b, ga, gb, gain_idx, sa,
+                       inv_norm_dim, eps, rd);
+  };
+  auto by_chunks = [&](auto c_tag) {
+    constexpr int C = decltype(c_tag)::value;
+    using One = std::integral_constant<int, 1>;
+    using Two = std::integral_constant<int, 2>;
+    if (nseg == 1) {
+      launch(c_tag, One{}, off0, 0, g0, nullptr, scale0);
+      return;
+    }
+    if constexpr (C <= 8) {
+      launch(c_tag, Two{}, off0, off1, g0, g1, scale0);
+    } else {
+      launch(c_tag, One{}, off0, 0, g0, nullptr, scale0);
+      launch(c_tag, One{}, off1, 0, g1, nullptr, 1.f);
+    }
+  };
   switch (chunks_per_lane<T>(a)) {
-    case 4: QK_LAUNCH(4); break;
-    case 8: QK_LAUNCH(8); break;
-    case 12: QK_LAUNCH(12); break;
-    case 16: QK_LAUNCH(16); break;
+    case 4: by_chunks(std::integral_constant<int, 4>{}); break;
+    case 8: by_chunks(std::integral_constant<int, 8>{}); break;
+    case 12: by_chunks(std::integral_constant<int, 12>{}); break;
+    case 16: by_chunks(std::integral_constant<int, 16>{}); break;
     default: return hipErrorInvalidValue;
   }
-#undef QK_LAUNCH
   return hipGetLastError();
 }
 
