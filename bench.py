@@ -35,8 +35,8 @@ ATTN_TRAFFIC = {
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
     "sha256": "0d151ab01e5d6347df331574888627d1934903d8fa92ccff9627be0697dd1de5",
-    "fetch_bytes": 1166123.8 * 1024 / 0.500,
-    "write_bytes": 392473.6 * 1024 / 1.000,
+    "fetch_bytes": 1166125.9 * 1024 / 0.500,
+    "write_bytes": 393418.9 * 1024 / 1.000,
 }
 
 
