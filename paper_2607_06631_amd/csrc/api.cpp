@@ -447,14 +447,16 @@ dif_status check_ws(const WsLayout& w, const void* ws, size_t bytes) {
 template <typename T, typename OutT>
 dif_status gemm(int kind, const T* A, int64_t lda, const T* Bm, int64_t ldb, OutT* C, int64_t ldc,
                 int M, int N, int K, int epi, const float* bias, const float* g0, const float* g1,
-                hipStream_t s, const dif::GemmGather* gather = nullptr) {
+                hipStream_t s, const dif::GemmGather* gather = nullptr,
+                const dif::GemmVt* vt = nullptr) {
   if (M <= 0 || N <= 0) return DIF_OK;
   const double es = sizeof(T);
   const double Nt = (double)N * (gather ? gather->nseg : 1);   // all segments
   const double bytes = ((double)M * K + Nt * K) * es + (double)M * Nt * sizeof(OutT) *
                                                           (epi == dif::EPI_RESIDUAL ? 2 : 1);
   ProfScope ps(kind, s, 2.0 * M * Nt * (double)K, bytes);
-  HIP_TRY((dif::launch_gemm<T, OutT>(A, lda, Bm, ldb, C, ldc, M, N, K, epi, bias, g0, g1, s, gather)));
+  HIP_TRY((dif::launch_gemm<T, OutT>(A, lda, Bm, ldb, C, ldc, M, N, K, epi, bias, g0, g1, s, gather,
+                                     vt)));
   return DIF_OK;
 }
 
@@ -560,6 +562,13 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       g_cross_k{nullptr, lp.at<int32_t>(lp.o_kch_cross), 0},
       g_ffn_k{nullptr, lp.at<int32_t>(lp.o_kch_ffn), 0};
   if (a > 0) {
+    // q and k go to `big` (row-major, for QK-norm in place); v is written
+    // transposed into vt [B, a, ldvt] by the same launch, as attention reads
+    // it, when the v columns start on a GEMM tile (always for head width 128
+    // and for indexed plans, where v is a launch segment of its own); else v
+    // is stored with q and k and transposed by its own kernel
+    const bool vt_in_gemm = ix || (2 * a) % 256 == 0;
+    const dif::GemmVt vtd{vt, wl.ldvt, 2 * a, a, L};
     if (ix) {
       dif::GemmGather g = g_self_rows;
       g.nseg = 3;
@@ -568,10 +577,11 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       g.seg_bias[0] = W.self_bk;
       g.seg_bias[1] = W.self_bv;
       DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, (const T*)W.self_wq, D, big, 3 * a, M, a, D,
-                          dif::EPI_STORE, W.self_bq, nullptr, nullptr, s, &g)));
+                          dif::EPI_STORE, W.self_bq, nullptr, nullptr, s, &g, &vtd)));
     } else {
       DIF_TRY((gemm<T, T>(PK_GEMM_QKV, xn, D, lp.at<T>(lp.o_wqkv), D, big, 3 * a, M, 3 * a, D,
-                          dif::EPI_STORE, lp.at<float>(lp.o_bqkv), nullptr, nullptr, s)));
+                          dif::EPI_STORE, lp.at<float>(lp.o_bqkv), nullptr, nullptr, s, nullptr,
+                          vt_in_gemm ? &vtd : nullptr)));
     }
     {
       ProfScope ps(PK_QK_NORM, s, 0, 4.0 * M * a * es);
@@ -581,7 +591,7 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
                                      ix ? W.self_gk : lp.at<float>(lp.o_gk), inv_d, c.eps, &rd, s,
                                      ix ? rs : nullptr, q_scale));
     }
-    {
+    if (!vt_in_gemm) {
       ProfScope ps(PK_TRANSPOSE, s, 0, 2.0 * M * a * es);
       HIP_TRY(dif::launch_transpose_vt<T>(big + 2 * a, 3 * a, a, B, L, vt, wl.ldvt, s));
     }

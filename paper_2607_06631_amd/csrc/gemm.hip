@@ -54,6 +54,12 @@ struct GemmParams {
   const int32_t* kch;    // GA_KCH
   int b_rows;            // GA_ROWS: rows of the union B matrix
   int vec4;              // C rows allow aligned 4-element accesses
+  // transposed output: columns from output column vt_col0 on go to
+  // vt[(b * vt_dims + col - vt_col0) * ldvt + j] for row m = b * vt_L + j
+  OutT* vt;
+  int64_t ldvt;
+  int vt_col0, vt_dims, vt_L;
+  int vt_vec4;           // vt rows allow aligned 4-element stores and vt_L % 4 == 0
 };
 
 // four consecutive output elements: 8-byte (bf16) or 16-byte (f32) accesses
@@ -290,6 +296,56 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
     }
   }
   constexpr int NPASS = (TM / 2) * (TN / 2);
+  // A tile whose columns start at or past vt_col0 stores transposed (the
+  // host keeps vt_col0 on a tile or segment boundary, so this is uniform).
+  if constexpr (EPI == EPI_STORE) {
+    if (p.vt && sg * p.N + n0 >= p.vt_col0) {
+      // staging [dim][token]: token bits 2.. are XORed with dim bits 0..3, so
+      // the column-wise writes of a 32-lane column group and the 16-byte
+      // reads of four consecutive tokens are both free of bank conflicts
+      auto tidx = [](int d, int t) { return d * 64 + (t ^ ((d & 15) << 2)); };
+#pragma unroll
+      for (int ps = 0; ps < NPASS; ++ps) {
+        const int rb = ps / (TN / 2), ch = ps % (TN / 2);
+#pragma unroll
+        for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+          for (int jj = 0; jj < 2; ++jj) {
+            const int i = 2 * rb + ii, j = 2 * ch + jj;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              stage[tidx(jj * 32 + col, ii * 32 + acc_row(r, g))] = acc[i][j][r] + colv[j];
+          }
+        __syncthreads();
+        const int q4 = lane & 15;                                    // 4-token group
+        const int m = m0 + wm * TM * 32 + rb * 64 + 4 * q4;          // its first token
+        const int bb = m / p.vt_L, jt = m - bb * p.vt_L;
+        const bool full4 = p.vt_vec4 && m + 4 <= p.M;                // same sample, aligned
+#pragma unroll
+        for (int t = 0; t < 16; ++t) {
+          const int dl = t * 4 + (lane >> 4);                        // dim within the pass
+          const int n = n0 + wn * TN * 32 + ch * 64 + dl;
+          const f32x4 sv = *reinterpret_cast<const f32x4*>(&stage[tidx(dl, 4 * q4)]);
+          if (n >= p.N || m >= p.M) continue;
+          const int dim = sg * p.N + n - p.vt_col0;
+          float v[4] = {sv[0], sv[1], sv[2], sv[3]};
+          if (full4) {
+            store4(p.vt + ((int64_t)bb * p.vt_dims + dim) * p.ldvt + jt, v);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int me = m + e;
+              if (me >= p.M) break;
+              const int be = me / p.vt_L, je = me - be * p.vt_L;
+              p.vt[((int64_t)be * p.vt_dims + dim) * p.ldvt + je] = from_f32<OutT>(v[e]);
+            }
+          }
+        }
+        if (ps + 1 < NPASS) __syncthreads();
+      }
+      return;
+    }
+  }
 #pragma unroll
   for (int ps = 0; ps < NPASS; ++ps) {
     const int rb = ps / (TN / 2), ch = ps % (TN / 2);   // 64-row block, 64-column half
@@ -358,7 +414,8 @@ void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
 template <typename T, typename OutT>
 hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
-                       const float* gate1, hipStream_t stream, const GemmGather* gather) {
+                       const float* gate1, hipStream_t stream, const GemmGather* gather,
+                       const GemmVt* vt) {
   if (M <= 0 || N <= 0) return hipSuccess;
   GemmParams<T, OutT> p{};
   p.A = A;
@@ -375,6 +432,22 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
   p.gate0 = gate0;
   p.gate1 = gate1;
   p.vec4 = (ldc % 4 == 0) && (reinterpret_cast<uintptr_t>(C) % (4 * sizeof(OutT)) == 0);
+  if (vt) {
+    // the transposed columns must start on a tile boundary (one B matrix) or
+    // at a segment, so every tile is wholly transposed or not
+    const int nseg = gather ? gather->nseg : 1;
+    const bool aligned = nseg > 1 ? vt->col0 % N == 0 : vt->col0 % BN_MAX == 0;
+    if (epi != EPI_STORE || !vt->vt || vt->L <= 0 || vt->dims <= 0 || vt->ldvt < vt->L || !aligned ||
+        vt->col0 < 0 || vt->col0 + vt->dims > nseg * N || M % vt->L != 0)
+      return hipErrorInvalidValue;
+    p.vt = static_cast<OutT*>(vt->vt);
+    p.ldvt = vt->ldvt;
+    p.vt_col0 = vt->col0;
+    p.vt_dims = vt->dims;
+    p.vt_L = vt->L;
+    p.vt_vec4 = vt->L % 4 == 0 && vt->ldvt % 4 == 0 &&
+                reinterpret_cast<uintptr_t>(vt->vt) % (4 * sizeof(OutT)) == 0;
+  }
   if (gather && gather->nseg > 1) {
     if (gather->nseg > kMaxSeg || epi == EPI_RESIDUAL) return hipErrorInvalidValue;
     p.nseg = gather->nseg;
@@ -415,7 +488,8 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
 #define INST(T, OutT)                                                                         \
   template hipError_t launch_gemm<T, OutT>(const T*, int64_t, const T*, int64_t, OutT*, int64_t, \
                                            int, int, int, int, const float*, const float*,    \
-                                           const float*, hipStream_t, const GemmGather*);
+                                           const float*, hipStream_t, const GemmGather*,      \
+                                           const GemmVt*);
 INST(bf16, bf16)
 INST(bf16, float)
 INST(float, float)

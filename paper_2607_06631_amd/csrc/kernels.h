@@ -28,11 +28,23 @@ struct GemmGather {
   const float* seg_bias[2] = {nullptr, nullptr};
 };
 
+// Transposed output for the columns of a store-epilogue GEMM from output
+// column col0 on (col0 on a 256-column tile boundary, or the first column of
+// a segment): column col0 + d of row m = b * L + j goes to
+// vt[(b * dims + d) * ldvt + j].  Used to write V^T straight from the QKV
+// projection.
+struct GemmVt {
+  void* vt;
+  int64_t ldvt;
+  int col0, dims, L;
+};
+
 // C[M,N] = epi(A[M,K] * B[N,K]^T); T in {float, __bf16}; OutT in {T, float}.
 template <typename T, typename OutT>
 hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C, int64_t ldc,
                        int M, int N, int K, int epi, const float* bias, const float* gate0,
-                       const float* gate1, hipStream_t stream, const GemmGather* gather = nullptr);
+                       const float* gate1, hipStream_t stream, const GemmGather* gather = nullptr,
+                       const GemmVt* vt = nullptr);
 
 // Flash attention; V given transposed (see dif_attention in dif.h).
 // q_scaled: Q already multiplied by log2(e)/sqrt(head_dim).
