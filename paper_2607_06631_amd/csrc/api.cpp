@@ -228,6 +228,7 @@ struct dif_model {
   dif_config cfg;
   dif_weights w;
   std::vector<dif_layer_weights> layers;
+  int ncu = 0;   // compute units of the device the model was created on
 };
 
 struct dif_plan {
@@ -367,7 +368,7 @@ Layout build_layout(const dif_model* m, const dif_step_masks* mk, bool indexed) 
 // workspace layout
 // ---------------------------------------------------------------------------
 struct WsLayout {
-  size_t xn, big, vt, o, ckv, cvt, x, zc, e, e0, t1, t2, emb, total;
+  size_t xn, big, vt, o, ckv, cvt, x, zc, e, e0, t1, t2, emb, part, total;
   int64_t ldvt, ldcvt;
 };
 
@@ -392,6 +393,7 @@ WsLayout ws_layout(const dif_config& c, int B, int L, int Lc) {
   w.t1 = cv.take(std::max<size_t>(D, c.freq_dim) * 4);
   w.t2 = cv.take(std::max<size_t>(D, c.freq_dim) * 4);
   w.emb = cv.take(c.freq_dim * 4);
+  w.part = cv.take(dif::attention_split_bytes(c.head_dim));   // self-attention key splits
   w.total = cv.off;
   return w;
 }
@@ -463,12 +465,14 @@ dif_status gemm(int kind, const T* A, int64_t lda, const T* Bm, int64_t ldb, Out
 template <typename T>
 dif_status attention(int kind, int dh, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                      const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk, int H,
-                     hipStream_t s, bool q_scaled = false) {
+                     hipStream_t s, bool q_scaled = false, float* split_part = nullptr,
+                     int ncu = 0) {
   if (H <= 0) return DIF_OK;
   const double flops = 4.0 * B * (double)Lq * Lk * dh * H;
   const double bytes = (double)B * (2.0 * Lq + 2.0 * Lk) * H * dh * sizeof(T);
   ProfScope ps(kind, s, flops, bytes);
-  HIP_TRY(dif::launch_attention<T>(dh, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk, H, s, q_scaled));
+  HIP_TRY(dif::launch_attention<T>(dh, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk, H, s, q_scaled,
+                                   split_part, ncu));
   return DIF_OK;
 }
 
@@ -596,7 +600,8 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       HIP_TRY(dif::launch_transpose_vt<T>(big + 2 * a, 3 * a, a, B, L, vt, wl.ldvt, s));
     }
     DIF_TRY(attention<T>(PK_ATTN_SELF, dh, big, 3 * a, big + a, 3 * a, vt, wl.ldvt, o, a, B, L, L,
-                         lp.info.self_heads, s, true));
+                         lp.info.self_heads, s, true, reinterpret_cast<float*>(ws + wl.part),
+                         m->ncu));
   }
   if (ix)
     DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), (const T*)W.self_wo, D, x, D, M, D, a,
@@ -900,8 +905,12 @@ dif_status dif_model_create(const dif_config* cfg, const dif_weights* w, dif_mod
       if (!p) return fail(DIF_E_ARG, "layer %d has a null weight pointer", l);
   }
   if (!is_gfx950()) return fail(DIF_E_UNSUPPORTED, "current HIP device is not gfx950");
+  int dev = 0, ncu = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
   dif_model* m = new dif_model();
   m->cfg = *cfg;
+  m->ncu = ncu;
   m->w = *w;
   m->layers.assign(w->layers, w->layers + cfg->n_layers);
   m->w.layers = nullptr;

@@ -40,6 +40,7 @@ namespace dif {
 // sequences (the text tokens), where eight waves leave too few workgroups and
 // too few key tiles to amortise each workgroup's prologue
 constexpr int kLongKeys = 4096;
+constexpr int kMaxSplitItems = 128;   // split items one workspace region holds
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
 
@@ -52,7 +53,23 @@ struct AttnParams {
   int64_t ldq, ldk, ldvt, ldo;
   int B, Lq, Lk, H;
   float c;  // log2(e) / sqrt(head_dim)
+  // Work items (query block, head, sample) [0, nreg) run whole; items from
+  // nreg on are split along the keys at tile split_tile, each half writing
+  // its unnormalised output and (m, l) to part for attn_merge_kernel.
+  int nreg, split_tile;
+  float* part;
 };
+
+// Partial-result layout of a split item s and key half k (0, 1), for BMQ
+// queries: [s][k][BMQ][DH] output sums, then [s][k][BMQ][2] (m, l).
+template <int DH>
+__host__ __device__ inline size_t part_o_off(int s, int k, int q, int bmq) {
+  return ((size_t)(2 * s + k) * bmq + q) * DH;
+}
+template <int DH>
+__host__ __device__ inline size_t part_ml_off(int nsplit, int s, int k, int q, int bmq) {
+  return (size_t)2 * nsplit * bmq * DH + ((size_t)(2 * s + k) * bmq + q) * 2;
+}
 
 // LDS row of key kappa (0..31) inside a 32-key sub-tile.
 __device__ __forceinline__ int key_slot(int kappa) {
@@ -82,7 +99,18 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
   const int g = lane >> 5, col = lane & 31;
 
   const int nqb = (p.Lq + BMQ - 1) / BMQ;
-  const int bid = xcd_remap(blockIdx.x, nqb * p.H * p.B);
+  const int ntiles = (p.Lk + AT_BN - 1) / AT_BN;
+  // this workgroup's item and key-tile range [t0, t1)
+  int bid, split = -1, t0 = 0, t1 = ntiles;
+  if ((int)blockIdx.x < p.nreg) {
+    bid = xcd_remap(blockIdx.x, p.nreg);
+  } else {
+    const int sidx = (int)blockIdx.x - p.nreg;   // dispatched last: the final round
+    bid = p.nreg + (sidx >> 1);
+    split = sidx;
+    if (sidx & 1) t0 = p.split_tile;
+    else t1 = p.split_tile;
+  }
   const int qb = bid % nqb, hb = bid / nqb;
   const int h = hb % p.H, b = hb / p.H;
 
@@ -98,7 +126,6 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
 
   const T* kbase = p.K + (int64_t)b * p.Lk * p.ldk + h * DH;
   const T* vbase = p.Vt + ((int64_t)b * p.H + h) * DH * p.ldvt;
-  const int ntiles = (p.Lk + AT_BN - 1) / AT_BN;
 
   // Full tiles are copied straight into LDS with buffer loads (no staging
   // registers): each wave instruction fills 1 KB of LDS, lane l writing
@@ -219,12 +246,12 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
       if (key + 16 * g + r >= p.Lk) s[r] = -INFINITY;
   };
 
-  load_tile(0, 0);
+  load_tile(t0, 0);
   wait_vmcnt<0>();   // this wave's direct-to-LDS loads have landed
   __syncthreads();   // ... and every other wave's
 
-  // Initial base: the max of each query's first 32 scores (key 0 exists, so
-  // it is finite).  negm holds -m in MFMA output units.
+  // Initial base: the max of each query's first 32 scores of the range (its
+  // first key exists, so it is finite).  negm holds -m in MFMA output units.
   float m_run;
   f32x16 negm;
   {
@@ -232,7 +259,7 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
 #pragma unroll
     for (int r = 0; r < 16; ++r) z[r] = 0.f;
     f32x16 s0 = scores(0, 0, z);
-    if (p.Lk < 32) mask(s0, 0);
+    if (t0 * AT_BN + 32 > p.Lk) mask(s0, t0 * AT_BN);
     float mx = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s0[r]);
@@ -248,7 +275,7 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
     constexpr int buf = decltype(buf_c)::value;
     constexpr bool MASKED = decltype(masked_c)::value;
     // buffer buf^1 was last read before the previous barrier
-    if (kt + 1 < ntiles) load_tile(kt + 1, buf ^ 1);
+    if (kt + 1 < t1) load_tile(kt + 1, buf ^ 1);
 
     const int key0 = kt * AT_BN;
     // the two 32-key halves of the tile in turn: S^T, softmax, O^T += V^T P^T
@@ -328,20 +355,41 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
   };
   using B0 = std::integral_constant<int, 0>;
   using B1 = std::integral_constant<int, 1>;
-  const int nfull = p.Lk / AT_BN;   // tiles of 64 valid keys
-  int kt = 0;
+  const int nfull = min(p.Lk / AT_BN, t1);   // tiles of 64 valid keys in the range
+  int kt = t0;   // (t0 is even: buffer 0 holds tile t0)
   for (; kt + 2 <= nfull; kt += 2) {
     tile(kt, B0{}, std::false_type{});
     tile(kt + 1, B1{}, std::false_type{});
   }
   if (kt < nfull) tile(kt++, B0{}, std::false_type{});
-  if (kt < ntiles) {   // the partial last tile
-    if (kt & 1) tile(kt, B1{}, std::true_type{});
+  if (kt < t1) {   // the partial last tile
+    if ((kt - t0) & 1) tile(kt, B1{}, std::true_type{});
     else tile(kt, B0{}, std::true_type{});
   }
 
   const int q = qb * BMQ + wave * 32 + col;
   const float l = l_run + __shfl_xor(l_run, 32);
+  if (split >= 0) {
+    // unnormalised sums and this half's (m, l), combined by attn_merge_kernel
+    const int nsplit = (int)(gridDim.x - p.nreg) / 2;
+    const int ql = wave * 32 + col;
+    float* po = p.part + part_o_off<DH>(split >> 1, split & 1, ql, BMQ);
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rr + e];
+        *reinterpret_cast<f32x4*>(po + dt * 32 + 8 * rr + 4 * g) = v;
+      }
+    if (g == 0) {
+      float* pml = p.part + part_ml_off<DH>(nsplit, split >> 1, split & 1, ql, BMQ);
+      pml[0] = m_run;
+      pml[1] = l;
+    }
+    return;
+  }
   if (q >= p.Lq) return;
   const float inv = 1.f / l;
   T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
@@ -364,36 +412,86 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
     }
 }
 
+// Combines the two key halves of each split item: with m = max(m0, m1) and
+// a_k = 2^(m_k - m), O = (a0 O0 + a1 O1) / (a0 l0 + a1 l1).  One workgroup
+// per split item, a thread per four output dims of a query.
+template <typename T, int DH, int BMQ>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int nsplit) {
+  const int sidx = blockIdx.x;
+  const int nqb = (p.Lq + BMQ - 1) / BMQ;
+  const int item = p.nreg + sidx;
+  const int qb = item % nqb, hb = item / nqb;
+  const int h = hb % p.H, b = hb / p.H;
+  for (int idx = threadIdx.x; idx < BMQ * DH / 4; idx += 256) {
+    const int ql = idx / (DH / 4), d = (idx % (DH / 4)) * 4;
+    const int q = qb * BMQ + ql;
+    if (q >= p.Lq) continue;
+    const float* ml0 = p.part + part_ml_off<DH>(nsplit, sidx, 0, ql, BMQ);
+    const float* ml1 = p.part + part_ml_off<DH>(nsplit, sidx, 1, ql, BMQ);
+    const float m = fmaxf(ml0[0], ml1[0]);
+    const float a0 = __builtin_amdgcn_exp2f(ml0[0] - m), a1 = __builtin_amdgcn_exp2f(ml1[0] - m);
+    const float inv = 1.f / (a0 * ml0[1] + a1 * ml1[1]);
+    const f32x4 o0 = *reinterpret_cast<const f32x4*>(p.part + part_o_off<DH>(sidx, 0, ql, BMQ) + d);
+    const f32x4 o1 = *reinterpret_cast<const f32x4*>(p.part + part_o_off<DH>(sidx, 1, ql, BMQ) + d);
+    T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH + d;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) dst[e] = from_f32<T>((a0 * o0[e] + a1 * o1[e]) * inv);
+  }
+}
+
 template <typename T, int DH, int W>
-void launch_w(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
+void launch_w(AttnParams<T> p, bool q_scaled, hipStream_t stream, int ncu) {
   constexpr int BMQ = W * 32;
-  const int blocks = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
+  const int items = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
+  // Workgroups fill a CU (W = 8) or half of one (W = 4).  When the last
+  // round of workgroups would be at most half full, its items are split
+  // along the keys into two halves each, so the round is full and half as
+  // long; a merge pass combines the halves.
+  const int slots = ncu * (W == 8 ? 1 : 2);
+  const int rem = slots > 0 ? items % slots : 0;
+  const int nfull = p.Lk / AT_BN;
+  int nsplit = 0;
+  if (p.part && rem > 0 && 2 * rem <= slots && rem <= kMaxSplitItems && nfull >= 4 && BMQ <= 256)
+    nsplit = rem;
+  p.nreg = items - nsplit;
+  p.split_tile = (nfull / 2) & ~1;
+  const int blocks = p.nreg + 2 * nsplit;
   if (q_scaled)
     hipLaunchKernelGGL((flash_attn_kernel<T, DH, true, W>), dim3(blocks), dim3(64 * W), 0, stream, p);
   else
     hipLaunchKernelGGL((flash_attn_kernel<T, DH, false, W>), dim3(blocks), dim3(64 * W), 0, stream, p);
+  if (nsplit > 0)
+    hipLaunchKernelGGL((attn_merge_kernel<T, DH, BMQ>), dim3(nsplit), dim3(256), 0, stream, p, nsplit);
 }
 
 template <typename T, int DH>
-void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream) {
+void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream, int ncu) {
   // (float32 keeps four waves: its head-128 kernel needs one wave per SIMD)
-  if (sizeof(T) == 2 && p.Lk >= kLongKeys)
-    launch_w<T, DH, 8>(p, q_scaled, stream);
-  else
-    launch_w<T, DH, 4>(p, q_scaled, stream);
+  if constexpr (sizeof(T) == 2) {
+    if (p.Lk >= kLongKeys) {
+      launch_w<T, DH, 8>(p, q_scaled, stream, ncu);
+      return;
+    }
+  }
+  launch_w<T, DH, 4>(p, q_scaled, stream, ncu);
+}
+
+size_t attention_split_bytes(int head_dim) {
+  return (size_t)2 * kMaxSplitItems * 256 * (head_dim + 2) * sizeof(float);
 }
 
 template <typename T>
 hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                             const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk,
-                            int H, hipStream_t stream, bool q_scaled) {
+                            int H, hipStream_t stream, bool q_scaled, float* split_part,
+                            int ncu) {
   if (B <= 0 || Lq <= 0 || H <= 0) return hipSuccess;
   AttnParams<T> p{Q, K, Vt, O, ldq, ldk, ldvt, ldo, B, Lq, Lk, H,
-                  1.4426950408889634f / sqrtf((float)head_dim)};
+                  1.4426950408889634f / sqrtf((float)head_dim), 0, 0, split_part};
   if (head_dim == 128) {
-    launch_dh<T, 128>(p, q_scaled, stream);
+    launch_dh<T, 128>(p, q_scaled, stream, ncu);
   } else if (head_dim == 64) {
-    launch_dh<T, 64>(p, q_scaled, stream);
+    launch_dh<T, 64>(p, q_scaled, stream, ncu);
   } else {
     return hipErrorInvalidValue;
   }
@@ -402,9 +500,9 @@ hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, i
 
 template hipError_t launch_attention<bf16>(int, const bf16*, int64_t, const bf16*, int64_t,
                                            const bf16*, int64_t, bf16*, int64_t, int, int, int,
-                                           int, hipStream_t, bool);
+                                           int, hipStream_t, bool, float*, int);
 template hipError_t launch_attention<float>(int, const float*, int64_t, const float*, int64_t,
                                             const float*, int64_t, float*, int64_t, int, int,
-                                            int, int, hipStream_t, bool);
+                                            int, int, hipStream_t, bool, float*, int);
 
 }  // namespace dif

@@ -47,11 +47,16 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
                        const GemmVt* vt = nullptr);
 
 // Flash attention; V given transposed (see dif_attention in dif.h).
-// q_scaled: Q already multiplied by log2(e)/sqrt(head_dim).
+// q_scaled: Q already multiplied by log2(e)/sqrt(head_dim).  With a scratch
+// region split_part of attention_split_bytes(head_dim) bytes and the device's
+// CU count, a final round of workgroups that would run at most half full is
+// split along the keys and merged by a second launch.
 template <typename T>
 hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, int64_t ldk,
                             const T* Vt, int64_t ldvt, T* O, int64_t ldo, int B, int Lq, int Lk,
-                            int H, hipStream_t stream, bool q_scaled = false);
+                            int H, hipStream_t stream, bool q_scaled = false,
+                            float* split_part = nullptr, int ncu = 0);
+size_t attention_split_bytes(int head_dim);
 
 // Row LayerNorm of x [M, D] then
 //   mode 0: y = xhat * (1 + p2 + p3) + (p0 + p1)      (AdaLN; p1/p3 may be null)

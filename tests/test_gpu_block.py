@@ -218,6 +218,28 @@ def test_wan14b_width_block_each_structure(mid14, step):
     assert err <= TOL["bf16"]
 
 
+def test_wan13b_width_block_attention_key_split():
+    """Self-attention whose last round of workgroups is split along the keys
+    and merged: 4551 tokens (18 query blocks of 256, the last ragged), 9 kept
+    heads, batch 2 -> 324 work items on 256 CUs, so the 68 items of the final
+    round run as two key halves each; the second half ends in a 7-key tile."""
+    cfg = get_config("wan1.3b_block").with_(name="split13", grid=(3, 37, 41), text_len=77, batch=2)
+    masks = synth.make_masks(cfg, 0)
+    heads = int(masks["self_head_keep"][0].sum())
+    items = -(-cfg.seq_len // 256) * heads * cfg.batch
+    assert 0 < items % 256 <= 128 and cfg.seq_len % 64 == 7
+    say(f"wan1.3b-width block L={cfg.seq_len} B={cfg.batch} heads={heads}: {items} attention items")
+    w = synth.make_weights(cfg, seed=3)
+    model = make_model(cfg, w)
+    x, ctx, e0 = _inputs(cfg, 9)
+    e0[5] = -w["layers"][0]["mod"][5]   # FFN gate 0: the attention branches dominate the update
+    got, _ = gpu_block(model, cfg, masks, 0, 0, x, ctx, e0)
+    ref = oracle_block(cfg, w["layers"][0], masks, 0, x, ctx, e0, dtype=np.float32)
+    err = rel_err(got, ref)
+    say(f"  rel err {err:.3e}")
+    assert err <= TOL["bf16"]
+
+
 def test_wan13b_width_block_sharp_attention():
     cfg = MID13.with_(batch=1)
     say("wan1.3b-width block, sharp attention (QK gains x2)")
