@@ -138,8 +138,9 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "bench.py runs on one GPU: this build has no multi-GPU path; "
-                                   "DESIGN.md describes how the step would shard over GPUs",
+        print(json.dumps({"error": "bench.py measures one GPU: the library has no multi-GPU path "
+                                   "(a step would shard over GPUs by sequence, with the kept "
+                                   "heads' keys and values all-gathered per layer)",
                           "n_gpus": args.gpus}))
         sys.exit(2)
 
