@@ -368,7 +368,7 @@ Layout build_layout(const dif_model* m, const dif_step_masks* mk, bool indexed) 
 // workspace layout
 // ---------------------------------------------------------------------------
 struct WsLayout {
-  size_t xn, big, vt, o, ckv, cvt, x, zc, e, e0, t1, t2, emb, part, total;
+  size_t xn, big, vt, o, ckv, cvt, x, zc, e, e0, t1, t2, emb, part, part_bytes, total;
   int64_t ldvt, ldcvt;
 };
 
@@ -393,7 +393,10 @@ WsLayout ws_layout(const dif_config& c, int B, int L, int Lc) {
   w.t1 = cv.take(std::max<size_t>(D, c.freq_dim) * 4);
   w.t2 = cv.take(std::max<size_t>(D, c.freq_dim) * 4);
   w.emb = cv.take(c.freq_dim * 4);
-  w.part = cv.take(dif::attention_split_bytes(c.head_dim));   // self-attention key splits
+  // self-attention key splits: bf16 self-attention over long keys only
+  const bool split = c.dtype == DIF_BF16 && L >= dif::kAttnLongKeys;
+  w.part = cv.take(split ? dif::attention_split_bytes(c.head_dim) : 0);
+  w.part_bytes = split ? dif::attention_split_bytes(c.head_dim) : 0;
   w.total = cv.off;
   return w;
 }
@@ -600,8 +603,8 @@ dif_status block_impl(const dif_plan* plan, int layer, T* x, const T* ctx, const
       HIP_TRY(dif::launch_transpose_vt<T>(big + 2 * a, 3 * a, a, B, L, vt, wl.ldvt, s));
     }
     DIF_TRY(attention<T>(PK_ATTN_SELF, dh, big, 3 * a, big + a, 3 * a, vt, wl.ldvt, o, a, B, L, L,
-                         lp.info.self_heads, s, true, reinterpret_cast<float*>(ws + wl.part),
-                         m->ncu));
+                         lp.info.self_heads, s, true,
+                         wl.part_bytes ? reinterpret_cast<float*>(ws + wl.part) : nullptr, m->ncu));
   }
   if (ix)
     DIF_TRY((gemm<T, T>(PK_GEMM_SELF_OUT, o, std::max(a, 8), (const T*)W.self_wo, D, x, D, M, D, a,

@@ -39,7 +39,7 @@ namespace dif {
 // waves per workgroup: 8 when the keys are long (bf16), 4 for short key
 // sequences (the text tokens), where eight waves leave too few workgroups and
 // too few key tiles to amortise each workgroup's prologue
-constexpr int kLongKeys = 4096;
+constexpr int kLongKeys = kAttnLongKeys;
 constexpr int kMaxSplitItems = 128;   // split items one workspace region holds
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale

@@ -57,6 +57,7 @@ hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, i
                             int H, hipStream_t stream, bool q_scaled = false,
                             float* split_part = nullptr, int ncu = 0);
 size_t attention_split_bytes(int head_dim);
+constexpr int kAttnLongKeys = 4096;   // from this key count on, bf16 attention runs 8 waves
 
 // Row LayerNorm of x [M, D] then
 //   mode 0: y = xhat * (1 + p2 + p3) + (p0 + p1)      (AdaLN; p1/p3 may be null)
