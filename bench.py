@@ -34,9 +34,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "9d9694e6a0a83cb651fe6601a16fdb6cf6353a518df670caab183eb4de6bcc4c",
-    "fetch_bytes": 1122462.5 * 1024 / 0.500,
-    "write_bytes": 429703.9 * 1024 / 1.000,
+    "sha256": "5ff35620f3e58b3ef6a133ca24869fe563c1761883c91083d417195d0e4a6dc7",
+    "fetch_bytes": 1122447.0 * 1024 / 0.500,
+    "write_bytes": 430544.2 * 1024 / 1.000,
 }
 
 
