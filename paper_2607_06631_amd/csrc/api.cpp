@@ -103,14 +103,14 @@ class ProfScope {
     if (!g_prof.on) return;
     std::lock_guard<std::mutex> lk(g_prof.mu);
     a_ = g_prof.take();
-    if (a_) hipEventRecord(a_, s_);
+    // a launch whose start event cannot be recorded is left out of the timing
+    if (a_ && hipEventRecord(a_, s_) != hipSuccess) a_ = nullptr;
   }
   ~ProfScope() {
     if (!a_) return;
     std::lock_guard<std::mutex> lk(g_prof.mu);
     hipEvent_t b = g_prof.take();
-    if (!b) return;
-    hipEventRecord(b, s_);
+    if (!b || hipEventRecord(b, s_) != hipSuccess) return;
     g_prof.recs.push_back({kind_, a_, b, flops_, bytes_});
   }
 
