@@ -354,8 +354,11 @@ typedef enum { DIF_EPI_STORE = 0, DIF_EPI_GELU = 1, DIF_EPI_RESIDUAL = 2 } dif_e
 
 /* C[M, N] (out_dtype) = epilogue(A[M, K] B[N, K]^T), A and B in `dtype`,
  * float32 accumulation.  K % 64 == 0 for BF16, K % 32 == 0 for F32; K may
- * be 0 (acc = 0).  lda, ldb, ldc in elements, multiples of 16 bytes;
- * bias [N] float32 or NULL.  out_dtype = dtype or DIF_F32. */
+ * be 0 (acc = 0).  Leading dimensions in elements: lda >= K and ldb >= K,
+ * multiples of 16 bytes; ldc >= N (rows of 4-element-aligned C take the
+ * vector path); 256 rows of A, B or C must span less than 2 GiB
+ * (DIF_E_SHAPE otherwise).  bias [N] float32 or NULL.  out_dtype = dtype
+ * or DIF_F32. */
 dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda,
                     const void* B, int64_t ldb, void* C, int64_t ldc,
                     int32_t M, int32_t N, int32_t K, int32_t epilogue, const float* bias,

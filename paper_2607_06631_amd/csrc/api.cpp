@@ -1244,6 +1244,10 @@ dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda
   if (M == 0 || N == 0) return DIF_OK;
   if (!C) return fail(DIF_E_ARG, "null output");
   if (ldc < N) return fail(DIF_E_SHAPE, "ldc < N");
+  // the kernels address 256-row blocks through 32-bit buffer descriptors
+  const int64_t oes = esize(out_dtype), kBlock = 256, kSpan = int64_t(1) << 31;
+  if (kBlock * ldc * oes >= kSpan || (K > 0 && kBlock * std::max(lda, ldb) * es >= kSpan))
+    return fail(DIF_E_SHAPE, "256 rows of a matrix span 2 GiB or more");
   if (K > 0) {  // A and B are read only when K > 0
     if (!A || !B) return fail(DIF_E_ARG, "null operand");
     if (lda < K || ldb < K) return fail(DIF_E_SHAPE, "leading dimension too small");

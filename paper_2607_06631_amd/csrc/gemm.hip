@@ -24,6 +24,8 @@
 //            shorten the reduction.  The chunk table is staged in LDS once.
 // Masked rows / chunks get an offset past the descriptor's range, which the
 // buffer load returns as zero.
+#include <type_traits>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -276,8 +278,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
   // residual and the stores are whole 128-byte (bf16) row segments.  The
   // staging layout flips column bit 5 every four rows, which keeps both the
   // column writes and the row reads free of bank conflicts.
+  // A wave only reads back what it staged itself, and a wave's LDS
+  // instructions execute in order, so between its writes and reads the
+  // staging needs no workgroup barrier, only a wavefront-scope fence that
+  // keeps the compiler from reordering them (and, unlike a barrier, does not
+  // wait for the wave's outstanding residual loads).
   static_assert(TM % 2 == 0 && TN % 2 == 0, "epilogue passes of 64 x 64 per wave");
   float* stage = reinterpret_cast<float*>(&smem[0][0][0]) + wave * (64 * 64);
+  auto wave_sync = [] {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  };
   auto sidx = [](int r, int c) { return r * 64 + (c ^ (((r >> 2) & 1) << 5)); };
   float colv[TN], gatev[TN];
 #pragma unroll
@@ -316,7 +327,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
             for (int r = 0; r < 16; ++r)
               stage[tidx(jj * 32 + col, ii * 32 + acc_row(r, g))] = acc[i][j][r] + colv[j];
           }
-        __syncthreads();
+        wave_sync();
         const int q4 = lane & 15;                                    // 4-token group
         const int m = m0 + wm * TM * 32 + rb * 64 + 4 * q4;          // its first token
         const int bb = m / p.vt_L, jt = m - bb * p.vt_L;
@@ -341,14 +352,57 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
             }
           }
         }
-        if (ps + 1 < NPASS) __syncthreads();
+        if (ps + 1 < NPASS) wave_sync();
       }
       return;
     }
   }
+  // Residual rows are requested ahead of the staging, every pass's rows up
+  // front for bf16 output (in flight through all of the staging), pass by
+  // pass for float output (whose rows would not fit in the registers left).
+  // Loaded row by row next to the stores, each load would wait for the
+  // previous row's store (the compiler cannot rule out that they overlap):
+  // one memory round trip per row.
+  typedef typename std::conditional<std::is_same<OutT, float>::value, f32x4, bf16x4>::type Out4;
+  constexpr bool RES = EPI == EPI_RESIDUAL;
+  constexpr int RES_AHEAD = RES && sizeof(Out4) == 8 ? NPASS : 1;
+  Out4 xres[RES_AHEAD][RES ? 16 : 1];
+  const __amdgpu_buffer_rsrc_t c_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      Csg + (int64_t)m0 * p.ldc, (short)0,
+      (uint32_t)((int64_t)min(BM, p.M - m0) * p.ldc * (int64_t)sizeof(OutT)), kRsrcWord3);
+  // unconditional buffer loads (an exact count of loads in flight lets the
+  // staging wait only for the bias and gate): rows past M fall outside the
+  // descriptor and lanes of the ragged path get an offset past it, both
+  // reading zero
+  auto load_res = [&](int ps, Out4* dst) {
+    const int rb = ps / (TN / 2), ch = ps % (TN / 2);
+    const int nb = n0 + wn * TN * 32 + ch * 64 + (lane & 15) * 4;
+    const bool full4 = p.vec4 && nb + 4 <= p.N;
+    // (a select, not a branch per load; kMasked plus a row offset inside the
+    // tile stays past the descriptor, which the host keeps below kMasked)
+    const uint32_t base = full4 ? (uint32_t)nb * (uint32_t)sizeof(OutT) : kMasked;
+    const uint32_t row_bytes = (uint32_t)p.ldc * (uint32_t)sizeof(OutT);
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const int rt = wm * TM * 32 + rb * 64 + t * 4 + (lane >> 4);   // row within the tile
+      const uint32_t off = base + (uint32_t)rt * row_bytes;
+      if constexpr (sizeof(Out4) == 8)
+        dst[t] = __builtin_bit_cast(Out4, __builtin_amdgcn_raw_buffer_load_b64(c_rsrc, off, 0, 0));
+      else
+        dst[t] = __builtin_bit_cast(Out4, __builtin_amdgcn_raw_buffer_load_b128(c_rsrc, off, 0, 0));
+    }
+  };
+  if constexpr (RES && RES_AHEAD == NPASS) {
+#pragma unroll
+    for (int ps = 0; ps < NPASS; ++ps) load_res(ps, xres[ps]);
+  }
 #pragma unroll
   for (int ps = 0; ps < NPASS; ++ps) {
     const int rb = ps / (TN / 2), ch = ps % (TN / 2);   // 64-row block, 64-column half
+    const int cq = lane & 15;                          // 4-column chunk of the row
+    const int nb = n0 + wn * TN * 32 + ch * 64 + cq * 4;
+    const bool full4 = p.vec4 && nb + 4 <= p.N;
+    if constexpr (RES && RES_AHEAD == 1) load_res(ps, xres[0]);
 #pragma unroll
     for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
@@ -362,10 +416,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
           stage[sidx(ii * 32 + acc_row(r, g), jj * 32 + col)] = v;
         }
       }
-    __syncthreads();
-    const int cq = lane & 15;                          // 4-column chunk of the row
-    const int nb = n0 + wn * TN * 32 + ch * 64 + cq * 4;
-    const bool full4 = p.vec4 && nb + 4 <= p.N;
+    wave_sync();
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
       const int rl = t * 4 + (lane >> 4);              // row within the pass
@@ -376,10 +427,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
       OutT* dst = Csg + (int64_t)m * p.ldc + nb;
       if (full4) {
         if constexpr (EPI == EPI_RESIDUAL) {
-          float xr[4];
-          load4(dst, xr);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) v[e] += xr[e];
+          for (int e = 0; e < 4; ++e) v[e] += (float)xres[RES_AHEAD == 1 ? 0 : ps][t][e];
         }
         store4(dst, v);
       } else {
@@ -391,7 +440,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, O
           }
       }
     }
-    if (ps + 1 < NPASS) __syncthreads();   // reads done before the next pass overwrites
+    if (ps + 1 < NPASS) wave_sync();   // reads done before the next pass overwrites
   }
 }
 
@@ -417,6 +466,12 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
                        const float* gate1, hipStream_t stream, const GemmGather* gather,
                        const GemmVt* vt) {
   if (M <= 0 || N <= 0) return hipSuccess;
+  // 256-row blocks of A, B and C are addressed through 32-bit buffer
+  // descriptors whose offsets from kMasked on read as zero
+  if ((int64_t)BN_MAX * lda * (int64_t)sizeof(T) >= (int64_t)kMasked ||
+      (int64_t)BN_MAX * ldb * (int64_t)sizeof(T) >= (int64_t)kMasked ||
+      (int64_t)BN_MAX * ldc * (int64_t)sizeof(OutT) >= (int64_t)kMasked)
+    return hipErrorInvalidValue;
   GemmParams<T, OutT> p{};
   p.A = A;
   p.Bs[0] = B;

@@ -94,6 +94,13 @@ def test_op_entry_points_reject_bad_arguments(lib):
     # rejected on the host before any device work
     assert lib.dif_gemm(5, 0, None, 0, None, 0, None, 0, 1, 1, 64, 0, None, None, None, None) == -1
     assert lib.dif_gemm(0, 0, None, 64, None, 64, None, 64, 4, 4, 48, 0, None, None, None, None) == -2
+    # 256 rows of C (bf16, ldc = 2^22) or of A (lda = 2^22) span 2 GiB: more than
+    # the kernels' 32-bit buffer descriptors address (the pointer is never used)
+    fake = C.c_void_p(0x1000)
+    big = 1 << 22
+    assert lib.dif_gemm(0, 0, None, 64, None, 64, fake, big, 4, 4, 64, 0, None, None, None, None) == -2
+    assert lib.dif_gemm(0, 0, None, big, None, 64, fake, 64, 4, 4, 64, 0, None, None, None, None) == -2
+    assert b"2 GiB" in lib.dif_last_error()
     assert lib.dif_attention(0, 96, None, 0, None, 0, None, 0, None, 0, 1, 1, 1, 1, None) == -4
     assert lib.dif_attention(0, 128, None, 0, None, 0, None, 0, None, 0, 1, 1, 0, 1, None) == -2
     assert lib.dif_euler(None, None, 1.0, 0.5, 4, None) == -1
