@@ -91,7 +91,7 @@ __device__ __forceinline__ void store4(float* p, const float* v) {
 // WGM x WGN waves; each wave owns TM x TN MFMA 32x32 tiles; two LDS stages of
 // BKC 16-byte chunks per operand row.
 template <typename T, typename OutT, int EPI, int GA, int WGM, int WGN, int TM, int TN, int BKC>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_nt_kernel(GemmParams<T, OutT> p) {
+__global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kernel(GemmParams<T, OutT> p) {
   constexpr int NW = WGM * WGN;
   constexpr int NT = 64 * NW;
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
@@ -450,14 +450,28 @@ constexpr int kMaxKChunks = (160 * 1024 - 2 * 512 * G_BKC * 16) / 4;
 
 // 256 x 256 workgroup tile as 8 waves (2 x 4) of 128 x 64.
 constexpr int G_WGM = 2, G_WGN = 4, G_TM = 4, G_TN = 2;
-template <typename T, typename OutT, int EPI, int GA>
-void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
-  constexpr int WGM = G_WGM, WGN = G_WGN, TM = G_TM, TN = G_TN;
+// Store-epilogue problems with fewer 256 x 256 tiles than half the CUs (the
+// 512 text tokens' K / V projection) take 128 x 128 tiles of 4 waves of
+// 64 x 64 instead, two workgroups per CU: four times the workgroups.
+constexpr int kSmallProblemTiles = 128;
+template <typename T, typename OutT, int EPI, int GA, int WGM, int WGN, int TM, int TN>
+void launch_cfg(const GemmParams<T, OutT>& p, hipStream_t stream) {
   constexpr int BM = WGM * TM * 32, BN = WGN * TN * 32;
   const int tiles = ((p.M + BM - 1) / BM) * ((p.N + BN - 1) / BN) * p.nseg;
   const size_t dyn = GA == GA_KCH ? (size_t)(p.K / Chunk<T>::VEC) * sizeof(uint32_t) : 0;
   hipLaunchKernelGGL((gemm_nt_kernel<T, OutT, EPI, GA, WGM, WGN, TM, TN, G_BKC>),
                      dim3(tiles), dim3(64 * WGM * WGN), dyn, stream, p);
+}
+template <typename T, typename OutT, int EPI, int GA>
+void launch_tile(const GemmParams<T, OutT>& p, hipStream_t stream) {
+  if constexpr (EPI == EPI_STORE) {
+    const int big = ((p.M + 255) / 256) * ((p.N + 255) / 256) * p.nseg;
+    if (big < kSmallProblemTiles) {
+      launch_cfg<T, OutT, EPI, GA, 2, 2, 2, 2>(p, stream);
+      return;
+    }
+  }
+  launch_cfg<T, OutT, EPI, GA, G_WGM, G_WGN, G_TM, G_TN>(p, stream);
 }
 
 template <typename T, typename OutT>
