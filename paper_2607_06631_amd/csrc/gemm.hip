@@ -2,17 +2,18 @@
 //
 // Both operands are K-contiguous (nn.Linear layout), which is exactly the
 // per-lane layout the MFMA operands want: every lane feeds a 16-byte run of
-// consecutive k.  Workgroup tile 256 x 256, k-tile 128 bytes per row (64
-// bf16 / 32 f32), split over a grid of waves that each own a block of
-// MFMA 32x32 tiles.  Operand tiles are copied global -> LDS by buffer loads
-// that write LDS directly (no staging registers, no LDS store
-// instructions), double-buffered (2 x 64 KB of the 160 KB LDS): tile kt+1
-// is requested while tile kt is computed.  The 16-byte chunks of each row
-// are XOR-swizzled (swz) so the 32-row fragment reads are bank-conflict
-// free; each lane fetches the chunk that the swizzle places in the LDS slot
-// its load writes.  Ragged M and N: rows past the matrix read as zero through
-// the descriptor bounds and stores are predicated; K must be a multiple of
-// the k-tile (the plan pads pruned widths to 64).
+// consecutive k. Workgroup tile 256 x 256 (128 x 128 for small problems),
+// k-tile 128 bytes per row (64 bf16 / 32 f32), split over a grid of waves
+// that each own a block of MFMA 32x32 tiles. Operand tiles are copied
+// global -> LDS by buffer loads that write LDS directly (no staging
+// registers, no LDS store instructions), double-buffered (2 x 64 KB of the
+// 160 KB LDS at 256 x 256): tile kt+1 is requested while tile kt is
+// computed. The 16-byte chunks of each row are XOR-swizzled (swz) so the
+// 32-row fragment reads are bank-conflict free; each lane fetches the chunk
+// that the swizzle places in the LDS slot its load writes. Ragged M and N:
+// rows past the matrix read as zero through the descriptor bounds and
+// stores are predicated; K must be a multiple of the k-tile (the plan pads
+// pruned widths to 64).
 //
 // Index-table gather (the step's active parameters read in place from the
 // union weight set, no compacted copy):
