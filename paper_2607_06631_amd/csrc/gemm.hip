@@ -313,8 +313,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   if constexpr (EPI == EPI_STORE) {
     if (p.vt && sg * p.N + n0 >= p.vt_col0) {
       // staging [dim][token]: token bits 2.. are XORed with dim bits 0..3, so
-      // the column-wise writes of a 32-lane column group and the 16-byte
-      // reads of four consecutive tokens are both free of bank conflicts
+      // each lane's 16-byte writes of four consecutive tokens of one dim and
+      // the 16-byte reads of four consecutive tokens are both free of bank
+      // conflicts
       auto tidx = [](int d, int t) { return d * 64 + (t ^ ((d & 15) << 2)); };
 #pragma unroll
       for (int ps = 0; ps < NPASS; ++ps) {
@@ -324,9 +325,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
 #pragma unroll
           for (int jj = 0; jj < 2; ++jj) {
             const int i = 2 * rb + ii, j = 2 * ch + jj;
+            // registers 4q .. 4q+3 hold four consecutive tokens of one dim:
+            // one 16-byte write each
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              stage[tidx(jj * 32 + col, ii * 32 + acc_row(r, g))] = acc[i][j][r] + colv[j];
+            for (int q = 0; q < 4; ++q) {
+              f32x4 v;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + colv[j];
+              *reinterpret_cast<f32x4*>(&stage[tidx(jj * 32 + col, ii * 32 + acc_row(4 * q, g))]) = v;
+            }
           }
         wave_sync();
         const int q4 = lane & 15;                                    // 4-token group
