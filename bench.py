@@ -35,8 +35,8 @@ ATTN_TRAFFIC = {
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
     "sha256": "5ff35620f3e58b3ef6a133ca24869fe563c1761883c91083d417195d0e4a6dc7",
-    "fetch_bytes": 1122446.3 * 1024 / 0.500,
-    "write_bytes": 430027.2 * 1024 / 1.000,
+    "fetch_bytes": 1122453.0 * 1024 / 0.500,
+    "write_bytes": 429584.5 * 1024 / 1.000,
 }
 
 
