@@ -105,6 +105,27 @@ def test_gemm_ragged_columns_and_unaligned_rows(dtype, ldc_pad):
         assert np.all(out[:M, N:] == 7.0) and np.all(out[M] == 7.0)
 
 
+@pytest.mark.parametrize("M", [127 * 256 - 7, 127 * 256 + 37])
+def test_gemm_store_either_side_of_the_small_problem_tiling(M):
+    """Store-epilogue problems with fewer than 128 tiles of 256 x 256 run as
+    128 x 128 tiles: M = 32505 and 32549 with N = 256 give 127 and 128 large
+    tiles, one on each side of the switch; sampled rows incl. the ragged tail
+    against the float64 product."""
+    import torch
+    N, K = 256, 192
+    say(f"gemm store bf16 M={M} N={N} K={K}: {-(-M // 256) * (N // 256)} tiles of 256 x 256")
+    g = np.random.default_rng(M)
+    a, b = _rand(g, (M, K), 0.5), _rand(g, (N, K), 0.5)
+    bias = g.standard_normal(N).astype(np.float32)
+    C = torch.full((M, N), float("nan"), device="cuda", dtype=torch.float32)
+    B.dif_gemm(torch.from_numpy(a).cuda().to(torch.bfloat16), torch.from_numpy(b).cuda().to(torch.bfloat16),
+               C, B.EPI_STORE, bias=torch.from_numpy(bias).cuda())
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(64), g.choice(M, 512, replace=False), np.arange(M - 300, M)]))
+    ref = a[rows].astype(np.float64) @ b.astype(np.float64).T + bias
+    assert rel_err(to_np(C)[rows], ref) <= 1e-5
+
+
 def _attn_case(dtype, dh, H, Lq, Lk, Bn=1, qscale=1.0, seed=0):
     import torch
     g = np.random.default_rng(seed)
