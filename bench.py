@@ -164,7 +164,7 @@ def main():
     log(f"bench: weights ready ({time.perf_counter() - t_setup:.1f} s)")
     model = B.dif_model_create(cfg, w)
     masks = [synth.make_masks(cfg, s) for s in range(4)]
-    plans = [B.dif_plan_step(model, s, masks[s], kind=args.plan) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, cfg.timesteps[s], masks[s], kind=args.plan) for s in range(4)]
     plan_bytes = sum(p.mem.numel() for p in plans)
     gen = torch.Generator(device=dev)
     gen.manual_seed(1)

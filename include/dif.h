@@ -161,16 +161,29 @@ dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, s
  * columns [D, a], the same for cross-attention, kept W1 rows / b1 entries
  * and W2 columns zero-padded to a multiple of 64 channels.  Kept indices
  * are in ascending order.  `step` is the structure's index in the sampler
- * (0-based, < 4096), kept for the caller's bookkeeping.  plan_mem: caller
- * device memory of >= dif_plan_bytes bytes, 256-byte aligned, which must
- * stay valid until dif_plan_destroy.  The gather kernels and a small table
- * upload are enqueued on `stream`; the host index tables are owned by the
- * plan.  Errors: DIF_E_MASK, DIF_E_WORKSPACE (too small / misaligned),
- * DIF_E_HIP. */
-dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_masks* masks,
-                         void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out);
+ * (0-based, < 4096), kept for the caller's bookkeeping.
+ *
+ * t_s is the timestep the structure belongs to: the sampler pairs step i's
+ * structure g_{t_i} with its timestep t_i (Sec. 3.1 fixes the T = 4
+ * timesteps, Sec. 3.2 gives each of them its own gates).  The plan stores
+ * t_s, and dif_step_forward / dif_step_forward_cached / dif_rollout /
+ * dif_rollout_cached return DIF_E_ARG for any other timestep (exact float
+ * comparison) unless the plan was built with DIF_PLAN_ANY_T.  t_s must be
+ * finite (DIF_E_ARG) unless DIF_PLAN_ANY_T is set, where it is ignored.
+ *
+ * plan_mem: caller device memory of >= dif_plan_bytes bytes, 256-byte
+ * aligned, which must stay valid until dif_plan_destroy.  The gather
+ * kernels and a small table upload are enqueued on `stream`; the host index
+ * tables are owned by the plan.  Errors: DIF_E_ARG, DIF_E_MASK,
+ * DIF_E_WORKSPACE (too small / misaligned), DIF_E_HIP. */
+dif_status dif_plan_step(const dif_model* model, int32_t step, float t_s,
+                         const dif_step_masks* masks, void* plan_mem, size_t plan_bytes,
+                         dif_stream stream, dif_plan** out);
 
-/* Plan of either kind (DIF_PLAN_COMPACT is dif_plan_bytes / dif_plan_step).
+/* Plan flags of dif_plan_step_ex. */
+#define DIF_PLAN_ANY_T 1 /* the plan runs at any timestep (t_s is not checked) */
+
+/* Plan of either kind (DIF_PLAN_COMPACT with flags 0 is dif_plan_step).
  *
  * DIF_PLAN_INDEXED keeps only theta_union and the index tables I_t, as the
  * paper's inference engine does (Sec. 4.3, Fig. 2(c)): the GEMMs gather
@@ -184,13 +197,17 @@ dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_ma
  * compact plan's (exactly, when every chunk is wholly kept or dropped, as
  * with C = 8 gates).  Requires ffn_dim % 8 == 0 and ffn_dim <= 65536
  * (bf16) / 32768 (float32), else DIF_E_UNSUPPORTED.  The union weights
- * must stay valid and unchanged while the plan is used.  Other arguments,
- * ownership and errors as dif_plan_step; an unknown kind is DIF_E_ARG. */
+ * must stay valid and unchanged while the plan is used.  flags: 0 or
+ * DIF_PLAN_ANY_T (other bits: DIF_E_ARG).  Other arguments, ownership and
+ * errors as dif_plan_step; an unknown kind is DIF_E_ARG. */
 dif_status dif_plan_bytes_ex(const dif_model* model, const dif_step_masks* masks, int32_t kind,
                              size_t* bytes);
-dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step_masks* masks,
-                            int32_t kind, void* plan_mem, size_t plan_bytes, dif_stream stream,
-                            dif_plan** out);
+dif_status dif_plan_step_ex(const dif_model* model, int32_t step, float t_s,
+                            const dif_step_masks* masks, int32_t kind, int32_t flags,
+                            void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out);
+
+/* The timestep a plan is bound to and its flags (host only). */
+dif_status dif_plan_timestep(const dif_plan* plan, float* t_s, int32_t* flags);
 
 /* Frees the plan's host metadata only (plan_mem stays the caller's).  The
  * caller must synchronise `stream` before freeing plan_mem. */
@@ -219,7 +236,8 @@ dif_status dif_block_forward(const dif_plan* plan, int32_t layer, void* x, const
 
 /* One denoise step: model prediction v [B, L, Cp] (float32) for latents
  * z [B, L, Cp] (float32) at timestep t under the plan's structure:
- * timestep embedding, patch embedding, the N blocks, output head. */
+ * timestep embedding, patch embedding, the N blocks, output head.  t must
+ * be the plan's t_s unless the plan has DIF_PLAN_ANY_T (DIF_E_ARG). */
 dif_status dif_step_forward(const dif_plan* plan, const float* z, float t, const void* ctx,
                             int32_t B, int32_t L, int32_t Lc, float* v_out,
                             void* ws, size_t ws_bytes, dif_stream stream);
@@ -374,6 +392,37 @@ dif_status dif_attention(int32_t dtype, int32_t head_dim, const void* Q, int64_t
                          const void* K, int64_t ldk, const void* Vt, int64_t ldvt,
                          void* O, int64_t ldo, int32_t B, int32_t Lq, int32_t Lk,
                          int32_t n_heads, dif_stream stream);
+
+/* Flags of dif_attention_ex. */
+#define DIF_ATTN_Q_PRESCALED 1 /* Q already holds q * log2(e) / sqrt(head_dim) */
+
+/* Bytes of the split workspace dif_attention_ex may use (any Lq, Lk, B,
+ * n_heads).  DIF_E_UNSUPPORTED for a head_dim other than 64 / 128. */
+dif_status dif_attention_split_bytes(int32_t head_dim, size_t* bytes);
+
+/* dif_attention as the blocks launch it, for operator tests and
+ * benchmarks of that exact launch: the attention of the block's
+ * self-attention (softmax(Q K^T / sqrt(dh)) V, bidirectional, Sec. 3.2's
+ * pruned structure only changes n_heads).
+ *   flags & DIF_ATTN_Q_PRESCALED: Q holds the queries already multiplied by
+ *     log2(e)/sqrt(head_dim) (the block's QK-norm writes them so); the
+ *     kernel then takes its scores as base-2 exponents directly.  The result
+ *     is softmax(Q K^T ln 2) V for the given Q.  Other flag bits: DIF_E_ARG.
+ *   split_ws (device, >= dif_attention_split_bytes, 256-byte aligned) or
+ *     NULL: with a workspace, when the last round of workgroups on this
+ *     device would run at most half full, those work items run as two key
+ *     halves each whose partial sums a second kernel merges (as the blocks
+ *     do for bfloat16 with Lk >= 4096).  The result equals the unsplit
+ *     launch's up to float rounding.  Calls sharing a workspace must not
+ *     overlap.
+ * Every other argument, layout and error as dif_attention; DIF_E_WORKSPACE
+ * for a too small or misaligned split_ws; DIF_E_HIP if the device's compute
+ * unit count cannot be read. */
+dif_status dif_attention_ex(int32_t dtype, int32_t head_dim, int32_t flags, const void* Q,
+                            int64_t ldq, const void* K, int64_t ldk, const void* Vt, int64_t ldvt,
+                            void* O, int64_t ldo, int32_t B, int32_t Lq, int32_t Lk,
+                            int32_t n_heads, void* split_ws, size_t split_ws_bytes,
+                            dif_stream stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing: while enabled, every kernel the library launches is

@@ -83,10 +83,12 @@ def lib():
             "dif_model_create": (i32, [C.POINTER(DifConfig), C.POINTER(DifWeights), C.POINTER(vp)]),
             "dif_model_destroy": (i32, [vp]),
             "dif_plan_bytes": (i32, [vp, C.POINTER(DifStepMasks), C.POINTER(sz)]),
-            "dif_plan_step": (i32, [vp, i32, C.POINTER(DifStepMasks), vp, sz, vp, C.POINTER(vp)]),
+            "dif_plan_step": (i32, [vp, i32, f32, C.POINTER(DifStepMasks), vp, sz, vp,
+                                    C.POINTER(vp)]),
             "dif_plan_bytes_ex": (i32, [vp, C.POINTER(DifStepMasks), i32, C.POINTER(sz)]),
-            "dif_plan_step_ex": (i32, [vp, i32, C.POINTER(DifStepMasks), i32, vp, sz, vp,
+            "dif_plan_step_ex": (i32, [vp, i32, f32, C.POINTER(DifStepMasks), i32, i32, vp, sz, vp,
                                        C.POINTER(vp)]),
+            "dif_plan_timestep": (i32, [vp, C.POINTER(f32), C.POINTER(i32)]),
             "dif_plan_destroy": (i32, [vp]),
             "dif_plan_layer_info": (i32, [vp, i32, C.POINTER(DifLayerInfo)]),
             "dif_workspace_bytes": (i32, [vp, i32, i32, i32, C.POINTER(sz)]),
@@ -107,6 +109,9 @@ def lib():
                                          vp, sz, i32, i32, i32, vp, vp, sz, vp]),
             "dif_gemm": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp, vp, vp, vp]),
             "dif_attention": (i32, [i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32, i32, i32, vp]),
+            "dif_attention_split_bytes": (i32, [i32, C.POINTER(sz)]),
+            "dif_attention_ex": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32,
+                                       i32, i32, vp, sz, vp]),
             "dif_profile_enable": (i32, [i32]),
             "dif_profile_reset": (i32, []),
             "dif_profile_kind_name": (C.c_char_p, [i32]),
@@ -249,6 +254,7 @@ def dif_model_create(cfg, weights: Dict) -> Model:
 
 
 DIF_PLAN_COMPACT, DIF_PLAN_INDEXED = 0, 1
+DIF_PLAN_ANY_T = 1
 PLAN_KINDS = {"compact": DIF_PLAN_COMPACT, "indexed": DIF_PLAN_INDEXED}
 
 
@@ -259,10 +265,11 @@ def dif_plan_bytes(model: Model, masks, kind: str = "compact") -> int:
     return n.value
 
 
-def dif_plan_step(model: Model, step: int, masks, stream=None, kind: str = "compact") -> Plan:
+def dif_plan_step(model: Model, step: int, t_s: float, masks, stream=None, kind: str = "compact",
+                  any_t: bool = False) -> Plan:
     """Index tables (and, for kind="compact", the gather of the step's active
     parameters) in plan memory allocated here with torch (owned by the
-    returned Plan)."""
+    returned Plan).  The plan is bound to timestep t_s (any_t: unbound)."""
     import torch
     m = _Masks(masks)
     n = C.c_size_t()
@@ -270,11 +277,19 @@ def dif_plan_step(model: Model, step: int, masks, stream=None, kind: str = "comp
     _check(lib().dif_plan_bytes_ex(model.handle, C.byref(m.struct), k, C.byref(n)))
     mem = torch.empty(max(n.value, 256), dtype=torch.uint8, device="cuda")
     h = C.c_void_p()
-    _check(lib().dif_plan_step_ex(model.handle, step, C.byref(m.struct), k, mem.data_ptr(), n.value,
+    _check(lib().dif_plan_step_ex(model.handle, step, float(t_s), C.byref(m.struct), k,
+                                  DIF_PLAN_ANY_T if any_t else 0, mem.data_ptr(), n.value,
                                   _stream(stream), C.byref(h)))
     plan = Plan(model, h, mem, m, step)
     plan.kind = kind
     return plan
+
+
+def dif_plan_timestep(plan: Plan):
+    """(t_s, flags) of a plan."""
+    t, f = C.c_float(), C.c_int32()
+    _check(lib().dif_plan_timestep(plan.handle, C.byref(t), C.byref(f)))
+    return t.value, f.value
 
 
 def dif_workspace_bytes(model: Model, B: int, L: int, Lc: int) -> int:
@@ -447,6 +462,26 @@ def dif_attention(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim:
     _check(lib().dif_attention(_dt(Q), head_dim, Q.data_ptr(), ldq, K.data_ptr(), ldk,
                                Vt.data_ptr(), ldvt, O.data_ptr(), ldo, B, Lq, Lk, n_heads,
                                _stream(stream)))
+
+
+DIF_ATTN_Q_PRESCALED = 1
+
+
+def dif_attention_split_bytes(head_dim: int) -> int:
+    n = C.c_size_t()
+    _check(lib().dif_attention_split_bytes(head_dim, C.byref(n)))
+    return n.value
+
+
+def dif_attention_ex(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim: int,
+                     ldq: int, ldk: int, ldvt: int, ldo: int, flags: int = 0, split_ws=None,
+                     stream=None) -> None:
+    """dif_attention with flags (DIF_ATTN_Q_PRESCALED) and an optional split
+    workspace (a uint8 device tensor of >= dif_attention_split_bytes)."""
+    _check(lib().dif_attention_ex(_dt(Q), head_dim, flags, Q.data_ptr(), ldq, K.data_ptr(), ldk,
+                                  Vt.data_ptr(), ldvt, O.data_ptr(), ldo, B, Lq, Lk, n_heads,
+                                  _ptr(split_ws), 0 if split_ws is None else split_ws.numel(),
+                                  _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

@@ -234,6 +234,8 @@ struct dif_model {
 struct dif_plan {
   const dif_model* model = nullptr;
   int32_t step = 0;
+  float t_s = 0.f;       // the timestep this structure belongs to
+  int32_t flags = 0;     // DIF_PLAN_ANY_T: any timestep accepted
   Layout lay;
   std::vector<float> host_rope;
   char* mem = nullptr;
@@ -824,6 +826,9 @@ dif_status step_call(const dif_plan* plan, const float* z, float t, const void* 
   const dif_config& c = plan->model->cfg;
   if (!z || (!ctx && !cache) || !v_out) return fail(DIF_E_ARG, "null tensor argument");
   if (!std::isfinite(t)) return fail(DIF_E_ARG, "timestep is not finite");
+  if (!(plan->flags & DIF_PLAN_ANY_T) && t != plan->t_s)
+    return fail(DIF_E_ARG, "timestep %g differs from the plan's t_s = %g (step %d)", (double)t,
+                (double)plan->t_s, plan->step);
   const TextLayout tl = text_layout(c, B, Lc);
   if (cache) DIF_TRY(check_cache(tl, cache, cache_bytes));
   const WsLayout wl = ws_layout(c, B, L, Lc);
@@ -848,6 +853,9 @@ dif_status rollout_call(const dif_plan* const* plans, const float* timesteps, in
     if (!plans[i]) return fail(DIF_E_ARG, "plan %d is null", i);
     if (plans[i]->model != plans[0]->model) return fail(DIF_E_ARG, "plans of different models");
     if (!std::isfinite(timesteps[i])) return fail(DIF_E_ARG, "timestep %d is not finite", i);
+    if (!(plans[i]->flags & DIF_PLAN_ANY_T) && timesteps[i] != plans[i]->t_s)
+      return fail(DIF_E_ARG, "timestep %d = %g differs from its plan's t_s = %g", i,
+                  (double)timesteps[i], (double)plans[i]->t_s);
     if (sampler == DIF_SAMPLER_RENOISE && i + 1 < n_steps && (!eps || !eps[i]))
       return fail(DIF_E_ARG, "re-noise sampler needs eps[%d]", i);
   }
@@ -942,18 +950,23 @@ dif_status dif_plan_bytes(const dif_model* model, const dif_step_masks* masks, s
   return dif_plan_bytes_ex(model, masks, DIF_PLAN_COMPACT, bytes);
 }
 
-dif_status dif_plan_step(const dif_model* model, int32_t step, const dif_step_masks* masks,
-                         void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out) {
-  return dif_plan_step_ex(model, step, masks, DIF_PLAN_COMPACT, plan_mem, plan_bytes, stream, out);
+dif_status dif_plan_step(const dif_model* model, int32_t step, float t_s,
+                         const dif_step_masks* masks, void* plan_mem, size_t plan_bytes,
+                         dif_stream stream, dif_plan** out) {
+  return dif_plan_step_ex(model, step, t_s, masks, DIF_PLAN_COMPACT, 0, plan_mem, plan_bytes,
+                          stream, out);
 }
 
-dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step_masks* masks,
-                            int32_t kind, void* plan_mem, size_t plan_bytes, dif_stream stream,
-                            dif_plan** out) {
+dif_status dif_plan_step_ex(const dif_model* model, int32_t step, float t_s,
+                            const dif_step_masks* masks, int32_t kind, int32_t flags,
+                            void* plan_mem, size_t plan_bytes, dif_stream stream, dif_plan** out) {
   GUARD_BEGIN
   if (!model || !out) return fail(DIF_E_ARG, "null argument");
   *out = nullptr;
   if (step < 0 || step >= 4096) return fail(DIF_E_ARG, "step %d out of range", step);
+  if (flags & ~DIF_PLAN_ANY_T) return fail(DIF_E_ARG, "unknown plan flags 0x%x", flags);
+  if (!(flags & DIF_PLAN_ANY_T) && !std::isfinite(t_s))
+    return fail(DIF_E_ARG, "t_s is not finite (pass DIF_PLAN_ANY_T for an unbound plan)");
   DIF_TRY(check_plan_kind(&model->cfg, kind));
   DIF_TRY(check_masks(&model->cfg, masks));
   Layout lay = build_layout(model, masks, kind == DIF_PLAN_INDEXED);
@@ -966,6 +979,8 @@ dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step
   dif_plan* p = new dif_plan();
   p->model = model;
   p->step = step;
+  p->t_s = t_s;
+  p->flags = flags;
   p->lay = std::move(lay);
   p->mem = static_cast<char*>(plan_mem);
   p->bytes = plan_bytes;
@@ -1011,6 +1026,13 @@ dif_status dif_plan_step_ex(const dif_model* model, int32_t step, const dif_step
 
 dif_status dif_plan_destroy(dif_plan* plan) {
   delete plan;
+  return DIF_OK;
+}
+
+dif_status dif_plan_timestep(const dif_plan* plan, float* t_s, int32_t* flags) {
+  if (!plan || !t_s || !flags) return fail(DIF_E_ARG, "null argument");
+  *t_s = plan->t_s;
+  *flags = plan->flags;
   return DIF_OK;
 }
 
@@ -1268,14 +1290,29 @@ dif_status dif_gemm(int32_t dtype, int32_t out_dtype, const void* A, int64_t lda
   GUARD_END
 }
 
-dif_status dif_attention(int32_t dtype, int32_t head_dim, const void* Q, int64_t ldq, const void* K,
-                         int64_t ldk, const void* Vt, int64_t ldvt, void* O, int64_t ldo, int32_t B,
-                         int32_t Lq, int32_t Lk, int32_t n_heads, dif_stream stream) {
-  GUARD_BEGIN
+}  // extern "C"
+
+namespace {
+
+// Shared by dif_attention and dif_attention_ex: validation, then the launch
+// (split_ws null: unsplit).
+dif_status attention_call(int32_t dtype, int32_t head_dim, int32_t flags, const void* Q,
+                          int64_t ldq, const void* K, int64_t ldk, const void* Vt, int64_t ldvt,
+                          void* O, int64_t ldo, int32_t B, int32_t Lq, int32_t Lk,
+                          int32_t n_heads, float* split_ws, size_t split_ws_bytes,
+                          dif_stream stream) {
   if (dtype != DIF_BF16 && dtype != DIF_F32) return fail(DIF_E_ARG, "bad dtype");
   if (head_dim != 64 && head_dim != 128) return fail(DIF_E_UNSUPPORTED, "head_dim %d", head_dim);
+  if (flags & ~DIF_ATTN_Q_PRESCALED) return fail(DIF_E_ARG, "unknown attention flags 0x%x", flags);
   if (B < 0 || Lq < 0 || n_heads < 0) return fail(DIF_E_SHAPE, "negative size");
   if (Lk < 1) return fail(DIF_E_SHAPE, "Lk must be >= 1");
+  if (split_ws) {
+    if (reinterpret_cast<uintptr_t>(split_ws) % 256)
+      return fail(DIF_E_WORKSPACE, "split workspace not 256-byte aligned");
+    if (split_ws_bytes < dif::attention_split_bytes(head_dim))
+      return fail(DIF_E_WORKSPACE, "split workspace %zu bytes < required %zu", split_ws_bytes,
+                  dif::attention_split_bytes(head_dim));
+  }
   if (B == 0 || Lq == 0 || n_heads == 0) return DIF_OK;
   if (!Q || !K || !Vt || !O) return fail(DIF_E_ARG, "null tensor");
   const int64_t es = esize(dtype);
@@ -1286,12 +1323,51 @@ dif_status dif_attention(int32_t dtype, int32_t head_dim, const void* Q, int64_t
   if ((reinterpret_cast<uintptr_t>(Q) | reinterpret_cast<uintptr_t>(K) |
        reinterpret_cast<uintptr_t>(Vt) | reinterpret_cast<uintptr_t>(O)) % 16)
     return fail(DIF_E_ARG, "tensors must be 16-byte aligned");
+  int ncu = 0;
+  if (split_ws) {
+    int dev = 0;
+    HIP_TRY(hipGetDevice(&dev));
+    HIP_TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
+  }
+  const bool pre = (flags & DIF_ATTN_Q_PRESCALED) != 0;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   if (dtype == DIF_BF16)
     return attention<bf16>(PK_ATTN_SELF, head_dim, (const bf16*)Q, ldq, (const bf16*)K, ldk,
-                           (const bf16*)Vt, ldvt, (bf16*)O, ldo, B, Lq, Lk, n_heads, s);
+                           (const bf16*)Vt, ldvt, (bf16*)O, ldo, B, Lq, Lk, n_heads, s, pre,
+                           split_ws, ncu);
   return attention<float>(PK_ATTN_SELF, head_dim, (const float*)Q, ldq, (const float*)K, ldk,
-                          (const float*)Vt, ldvt, (float*)O, ldo, B, Lq, Lk, n_heads, s);
+                          (const float*)Vt, ldvt, (float*)O, ldo, B, Lq, Lk, n_heads, s, pre,
+                          split_ws, ncu);
+}
+
+}  // namespace
+
+extern "C" {
+
+dif_status dif_attention(int32_t dtype, int32_t head_dim, const void* Q, int64_t ldq, const void* K,
+                         int64_t ldk, const void* Vt, int64_t ldvt, void* O, int64_t ldo, int32_t B,
+                         int32_t Lq, int32_t Lk, int32_t n_heads, dif_stream stream) {
+  GUARD_BEGIN
+  return attention_call(dtype, head_dim, 0, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk, n_heads,
+                        nullptr, 0, stream);
+  GUARD_END
+}
+
+dif_status dif_attention_split_bytes(int32_t head_dim, size_t* bytes) {
+  if (!bytes) return fail(DIF_E_ARG, "null argument");
+  if (head_dim != 64 && head_dim != 128) return fail(DIF_E_UNSUPPORTED, "head_dim %d", head_dim);
+  *bytes = dif::attention_split_bytes(head_dim);
+  return DIF_OK;
+}
+
+dif_status dif_attention_ex(int32_t dtype, int32_t head_dim, int32_t flags, const void* Q,
+                            int64_t ldq, const void* K, int64_t ldk, const void* Vt, int64_t ldvt,
+                            void* O, int64_t ldo, int32_t B, int32_t Lq, int32_t Lk,
+                            int32_t n_heads, void* split_ws, size_t split_ws_bytes,
+                            dif_stream stream) {
+  GUARD_BEGIN
+  return attention_call(dtype, head_dim, flags, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk,
+                        n_heads, static_cast<float*>(split_ws), split_ws_bytes, stream);
   GUARD_END
 }
 

@@ -36,7 +36,7 @@ def oracle_block(cfg, wl, masks, layer, x, ctx, e0, rows=None, dtype=np.float64)
 
 def gpu_block(model, cfg, masks, step, layer, x, ctx, e0):
     import torch
-    plan = B.dif_plan_step(model, step, masks)
+    plan = B.dif_plan_step(model, step, cfg.timesteps[step], masks)
     xd, cd = to_dev(x, cfg), to_dev(ctx, cfg)
     ed = to_dev(e0, dtype=torch.float32)
     ws = B.workspace(model, x.shape[0], x.shape[1], ctx.shape[1])
@@ -133,7 +133,7 @@ def test_tiny_full_denoise_matches_oracle(tiny_model):
     cfg = TINY
     say("tiny 4-step denoise")
     masks = [synth.make_masks(cfg, s) for s in range(4)]
-    plans = [B.dif_plan_step(model, s, masks[s]) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, cfg.timesteps[s], masks[s]) for s in range(4)]
     z0 = synth.make_latents(cfg, seed=1)
     ctx = synth.make_context(cfg, seed=1)
     z = to_dev(z0, dtype=torch.float32)
@@ -185,7 +185,7 @@ def test_wan13b_width_step(mid13):
     cfg = MID13
     say("wan1.3b-width single-layer step forward")
     masks = synth.make_masks(cfg, 0)
-    plan = B.dif_plan_step(model, 0, masks)
+    plan = B.dif_plan_step(model, 0, 750, masks)
     z0 = synth.make_latents(cfg, seed=2)
     ctx = synth.make_context(cfg, seed=2)
     z = to_dev(z0, dtype=torch.float32)
@@ -271,7 +271,7 @@ def test_wan14b_width_step_with_block_skips():
     ctx = synth.make_context(cfg, seed=9)
     ref = O.step(z0, 500, ctx, w, masks, cfg)
     for kind in ("compact", "indexed"):
-        plan = B.dif_plan_step(model, 2, masks, kind=kind)
+        plan = B.dif_plan_step(model, 2, 500, masks, kind=kind)
         assert [plan.layer_info(l).block_keep for l in range(4)] == [1, 0, 1, 0]
         z = to_dev(z0, dtype=torch.float32)
         v = torch.empty_like(z)

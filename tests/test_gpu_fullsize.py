@@ -42,7 +42,7 @@ def _run(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="com
     w = synth.make_global_weights(one, 0)
     w["layers"] = [wl]
     model = make_model(one, w)
-    plan = B.dif_plan_step(model, 0, m1, kind=kind)
+    plan = B.dif_plan_step(model, 0, one.timesteps[0], m1, kind=kind)
     xd, cd = to_dev(x, one), to_dev(ctx, one)
     ed = to_dev(e0, dtype=torch.float32)
     ws = B.workspace(model, 1, one.seq_len, one.text_len)

@@ -33,7 +33,7 @@ def oracle_block(cfg, wl, masks, layer, x, ctx, e0):
 
 def run_block(model, cfg, masks, layer, x, ctx, e0, kind):
     import torch
-    plan = B.dif_plan_step(model, 0, masks, kind=kind)
+    plan = B.dif_plan_step(model, 0, cfg.timesteps[0], masks, kind=kind)
     xd, cd = to_dev(x, cfg), to_dev(ctx, cfg)
     ed = to_dev(e0, dtype=torch.float32)
     ws = B.workspace(model, x.shape[0], x.shape[1], ctx.shape[1])
@@ -118,7 +118,7 @@ def test_tiny_indexed_full_denoise(tiny_model):
     cfg = TINY
     say("tiny 4-step denoise, indexed plans")
     masks = [synth.make_masks(cfg, s) for s in range(4)]
-    plans = [B.dif_plan_step(model, s, masks[s], kind="indexed") for s in range(4)]
+    plans = [B.dif_plan_step(model, s, cfg.timesteps[s], masks[s], kind="indexed") for s in range(4)]
     z0 = synth.make_latents(cfg, seed=1)
     ctx = synth.make_context(cfg, seed=1)
     z = to_dev(z0, dtype=torch.float32)

@@ -46,7 +46,7 @@ def test_reordered_model_computes_the_same_block():
     e0 = synth.make_e0(cfg, 6, std=0.3)
     outs = []
     for m in (model, model_re):
-        plan = B.dif_plan_step(m, 0, masks)
+        plan = B.dif_plan_step(m, 0, cfg.timesteps[0], masks)
         xd = to_dev(x, cfg)
         ws = B.workspace(m, 1, cfg.seq_len, cfg.text_len)
         B.dif_block_forward(plan, 0, xd, to_dev(ctx, cfg), to_dev(e0, dtype=torch.float32), ws)

@@ -44,7 +44,7 @@ def test_rollout_renoise_matches_oracle(tiny, kind):
     import torch
     w, model, masks = tiny
     say(f"tiny 4-step rollout, re-noise sampler, {kind} plans")
-    plans = [B.dif_plan_step(model, s, masks[s], kind=kind) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, TINY.timesteps[s], masks[s], kind=kind) for s in range(4)]
     z0 = synth.make_latents(TINY, seed=11)
     ctx = synth.make_context(TINY, seed=11)
     eps = synth.make_renoise_eps(TINY, seed=11)
@@ -65,7 +65,7 @@ def test_rollout_from_an_intermediate_step(tiny):
     import torch
     w, model, masks = tiny
     say("tiny rollout from step 1")
-    plans = [B.dif_plan_step(model, s, masks[s]) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, TINY.timesteps[s], masks[s]) for s in range(4)]
     z0 = synth.make_latents(TINY, seed=12)
     ctx = synth.make_context(TINY, seed=12)
     eps = synth.make_renoise_eps(TINY, seed=12)
@@ -84,7 +84,7 @@ def test_rollout_euler_equals_step_by_step(tiny):
     import torch
     w, model, masks = tiny
     say("tiny Euler rollout vs step-by-step")
-    plans = [B.dif_plan_step(model, s, masks[s]) for s in range(4)]
+    plans = [B.dif_plan_step(model, s, TINY.timesteps[s], masks[s]) for s in range(4)]
     z0 = synth.make_latents(TINY, seed=13)
     ctx = to_dev(synth.make_context(TINY, seed=13), TINY)
     ws = B.workspace(model, 1, TINY.seq_len, TINY.text_len)

@@ -52,7 +52,7 @@ def test_wan14b_480p_stack_teacher_forced(stack, step):
     masks = synth.make_masks(cfg, step)
     say(f"step {step}: plan ({int(masks['self_head_keep'].sum())} self heads, "
         f"{int(masks['ffn_keep'].sum())} FFN channels over {cfg.n_layers} layers)")
-    plan = B.dif_plan_step(model, step, masks)
+    plan = B.dif_plan_step(model, step, cfg.timesteps[step], masks)
     gen = torch.Generator(device="cuda")
     gen.manual_seed(100 + step)
     z = torch.randn((L, Cp), generator=gen, device="cuda")

@@ -27,7 +27,7 @@ def tiny():
 
 def _step_pair(model, cfg, masks, kind, t, z0, ctx):
     import torch
-    plan = B.dif_plan_step(model, 0, masks, kind=kind)
+    plan = B.dif_plan_step(model, 0, t, masks, kind=kind)
     cd = to_dev(ctx, cfg)
     ws = B.workspace(model, z0.shape[0], cfg.seq_len, ctx.shape[1])
     cache = B.dif_text_cache_build(model, cd)
@@ -79,7 +79,7 @@ def test_tiny_cached_rollout_matches_oracle(tiny):
     w, model = tiny
     say("tiny cached 4-step rollout")
     masks = [synth.make_masks(TINY, s) for s in range(4)]
-    plans = [B.dif_plan_step(model, s, masks[s], kind="indexed") for s in range(4)]
+    plans = [B.dif_plan_step(model, s, TINY.timesteps[s], masks[s], kind="indexed") for s in range(4)]
     z0 = synth.make_latents(TINY, seed=90)
     ctx = synth.make_context(TINY, seed=90)
     eps = synth.make_renoise_eps(TINY, seed=90)
@@ -103,7 +103,7 @@ def test_cache_errors(tiny):
     _, model = tiny
     say("text cache argument errors")
     masks = synth.make_masks(TINY, 1)
-    plan = B.dif_plan_step(model, 1, masks)
+    plan = B.dif_plan_step(model, 1, 750.0, masks)
     cd = to_dev(synth.make_context(TINY, seed=1), TINY)
     cache = B.dif_text_cache_build(model, cd)
     z = torch.zeros(1, TINY.seq_len, TINY.patch_dim, device="cuda")
@@ -135,7 +135,7 @@ def test_wan14b_width_cached_block_batch_2(mid14, kind):
     x = synth.make_block_input(MID14, 5, scale=0.5)
     ctx = synth.make_context(MID14, 5)
     e0 = synth.make_e0(MID14, 5, std=0.3)
-    plan = B.dif_plan_step(model, 0, masks, kind=kind)
+    plan = B.dif_plan_step(model, 0, MID14.timesteps[0], masks, kind=kind)
     cd, ed = to_dev(ctx, MID14), to_dev(e0, dtype=torch.float32)
     ws = B.workspace(model, MID14.batch, MID14.seq_len, MID14.text_len)
     cache = B.dif_text_cache_build(model, cd)

@@ -395,6 +395,38 @@ def test_time_embedding_reshape_order():
     np.testing.assert_array_equal(e0[4], w["t_b3"][4 * cfg.dim:5 * cfg.dim])
 
 
+def test_time_embedding_matches_torch_modules():
+    """e = Linear2(SiLU(Linear1(emb))) and e0 = Linear3(SiLU(e)) reshaped to
+    [6, D], built from torch.nn modules loaded with the same weights, every
+    weight and bias non-zero: a dropped inner layer or SiLU, a transposed
+    matrix, a missing bias or a wrong reshape order fails here."""
+    cfg = MICRO
+    w = synth.make_weights(cfg, seed=4)
+    D, Fq = cfg.dim, cfg.freq_dim
+    for k in ("t_w1", "t_w2", "t_w3", "t_b1", "t_b2", "t_b3"):
+        assert np.all(w[k] != 0), k
+
+    def lin(wk, bk):
+        m = torch.nn.Linear(w[wk].shape[1], w[wk].shape[0], dtype=torch.float64)
+        with torch.no_grad():
+            m.weight.copy_(torch.from_numpy(w[wk].astype(np.float64)))
+            m.bias.copy_(torch.from_numpy(w[bk].astype(np.float64)))
+        return m
+
+    mlp = torch.nn.Sequential(lin("t_w1", "t_b1"), torch.nn.SiLU(), lin("t_w2", "t_b2"))
+    head = torch.nn.Sequential(torch.nn.SiLU(), lin("t_w3", "t_b3"), torch.nn.Unflatten(-1, (6, D)))
+    for t in (999.0, 750.0, 250.0, 0.0):
+        emb = torch.from_numpy(O.sinusoid(t, Fq))
+        with torch.no_grad():
+            e_ref = mlp(emb)
+            e0_ref = head(e_ref)
+        e, e0 = O.time_embedding(w, t)
+        np.testing.assert_allclose(e, e_ref.numpy(), rtol=0, atol=1e-12)
+        np.testing.assert_allclose(e0, e0_ref.numpy(), rtol=0, atol=1e-12)
+    # the modulation rows differ between timesteps (t reaches every row)
+    assert not np.allclose(O.time_embedding(w, 999.0)[1], O.time_embedding(w, 250.0)[1])
+
+
 def test_euler_and_sigma_schedule():
     sig = O.sigmas((999, 750, 500, 250))
     assert sig == [0.999, 0.75, 0.5, 0.25, 0.0]
