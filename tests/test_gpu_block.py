@@ -281,3 +281,24 @@ def test_wan14b_width_step_with_block_skips():
         err = rel_err(to_np(v), ref)
         say(f"  {kind}: rel err {err:.3e}")
         assert err <= TOL["bf16"]
+
+
+def test_step_rejects_a_timestep_other_than_the_plans(tiny_model):
+    """A plan is bound to its step's timestep (Sec. 3.1: the structure of
+    step i belongs to t_i); DIF_PLAN_ANY_T lifts the binding."""
+    import torch
+    w, model = tiny_model[0], tiny_model[1]
+    cfg = TINY
+    masks = synth.make_masks(cfg, 1)
+    plan = B.dif_plan_step(model, 1, cfg.timesteps[1], masks)
+    assert B.dif_plan_timestep(plan) == (float(cfg.timesteps[1]), 0)
+    z = torch.zeros((1, cfg.seq_len, cfg.patch_dim), device="cuda")
+    v = torch.empty_like(z)
+    ctx = to_dev(synth.make_context(cfg, seed=1), cfg)
+    ws = B.workspace(model, 1, cfg.seq_len, cfg.text_len)
+    with pytest.raises(B.DifError) as ei:
+        B.dif_step_forward(plan, z, cfg.timesteps[2], ctx, v, ws)
+    assert ei.value.code == -1
+    free = B.dif_plan_step(model, 1, float("nan"), masks, any_t=True)
+    B.dif_step_forward(free, z, cfg.timesteps[2], ctx, v, ws)
+    torch.cuda.synchronize()

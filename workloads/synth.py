@@ -137,6 +137,24 @@ def make_block_input(cfg: Config, seed: int = 0, scale: float = 1.0) -> np.ndarr
     return _store(cfg, x * np.float32(scale))
 
 
+def make_attention_inputs(L: int, n_heads: int, dh: int, q_std: float, k_std: float,
+                          seed: int = 0, heads=None, bf16: bool = True):
+    """q, k, v [L, len(heads) * dh] for attention operator tests, float32:
+    q ~ N(0, q_std^2), k ~ N(0, k_std^2), v ~ N(0, 1), rounded to bfloat16
+    when `bf16`.  Scores q.k / sqrt(dh) then have standard deviation
+    q_std * k_std.  Every head has its own stream, so any subset of heads
+    (default: all n_heads) is drawn identically on its own."""
+    hs = list(range(n_heads)) if heads is None else list(heads)
+    out = [np.empty((L, len(hs) * dh), dtype=np.float32) for _ in range(3)]
+    for i, h in enumerate(hs):
+        g = rng(SEED_INPUTS, seed, "attention", L, n_heads, dh, h)
+        cs = slice(i * dh, (i + 1) * dh)
+        out[0][:, cs] = _normal(g, (L, dh), q_std)
+        out[1][:, cs] = _normal(g, (L, dh), k_std)
+        out[2][:, cs] = _normal(g, (L, dh), 1.0)
+    return tuple(bf16_round(a) if bf16 else a for a in out)
+
+
 def make_e0(cfg: Config, seed: int = 0, std: float = 0.1) -> np.ndarray:
     """Synthetic per-step modulation e0 [6, D] for single-block tests."""
     g = rng(SEED_INPUTS, seed, cfg.name, "e0")
