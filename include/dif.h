@@ -424,6 +424,25 @@ dif_status dif_attention_ex(int32_t dtype, int32_t head_dim, int32_t flags, cons
                             int32_t n_heads, void* split_ws, size_t split_ws_bytes,
                             dif_stream stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * dif_attention_ex with its key-split workspace taken from a buffer the
+ * library keeps in static device memory, so the call allocates nothing.
+ * The buffer is DIF_ATTN_STATIC_SCRATCH_BYTES (32.5 MiB) on every device
+ * the library runs on, held until the process ends; it covers every problem
+ * size (the split needs a fixed-size workspace, at most that, for head_dim
+ * 64 and 128).  Every call on one device shares the buffer and leaves its
+ * contents behind (each launch writes every entry it reads, nothing needs
+ * clearing): calls that overlap on one device -- concurrent streams or host
+ * threads -- race, and the caller must serialise them.  Arguments, results
+ * and errors as dif_attention_ex with split_ws = the library's buffer;
+ * DIF_E_HIP if its device address cannot be obtained. */
+#define DIF_ATTN_STATIC_SCRATCH_BYTES ((size_t)34078720)
+dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flags, const void* Q,
+                                   int64_t ldq, const void* K, int64_t ldk, const void* Vt,
+                                   int64_t ldvt, void* O, int64_t ldo, int32_t B, int32_t Lq,
+                                   int32_t Lk, int32_t n_heads, dif_stream stream);
+
 /* ------------------------------------------------------------------------
  * Kernel timing: while enabled, every kernel the library launches is
  * bracketed by HIP events on its stream, grouped by kind, with the kind's

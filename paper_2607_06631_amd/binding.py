@@ -112,6 +112,8 @@ def lib():
             "dif_attention_split_bytes": (i32, [i32, C.POINTER(sz)]),
             "dif_attention_ex": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32, i32,
                                        i32, i32, vp, sz, vp]),
+            "dif_attention_ex_static": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32,
+                                              i32, i32, i32, vp]),
             "dif_profile_enable": (i32, [i32]),
             "dif_profile_reset": (i32, []),
             "dif_profile_kind_name": (C.c_char_p, [i32]),
@@ -482,6 +484,15 @@ def dif_attention_ex(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_d
                                   Vt.data_ptr(), ldvt, O.data_ptr(), ldo, B, Lq, Lk, n_heads,
                                   _ptr(split_ws), 0 if split_ws is None else split_ws.numel(),
                                   _stream(stream)))
+
+
+def dif_attention_ex_static(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim: int,
+                            ldq: int, ldk: int, ldvt: int, ldo: int, flags: int = 0,
+                            stream=None) -> None:
+    """dif_attention_ex with the library's static split workspace (allocates nothing)."""
+    _check(lib().dif_attention_ex_static(_dt(Q), head_dim, flags, Q.data_ptr(), ldq, K.data_ptr(),
+                                         ldk, Vt.data_ptr(), ldvt, O.data_ptr(), ldo, B, Lq, Lk,
+                                         n_heads, _stream(stream)))
 
 
 # ---------------------------------------------------------------------------

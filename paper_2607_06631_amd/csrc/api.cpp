@@ -1371,6 +1371,26 @@ dif_status dif_attention_ex(int32_t dtype, int32_t head_dim, int32_t flags, cons
   GUARD_END
 }
 
+dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flags, const void* Q,
+                                   int64_t ldq, const void* K, int64_t ldk, const void* Vt,
+                                   int64_t ldvt, void* O, int64_t ldo, int32_t B, int32_t Lq,
+                                   int32_t Lk, int32_t n_heads, dif_stream stream) {
+  GUARD_BEGIN
+  float* part = nullptr;
+  size_t bytes = 0;
+  const hipError_t e = dif::attention_static_scratch(&part, &bytes);
+  if (e != hipSuccess)
+    return fail(DIF_E_HIP, "static split workspace: %s", hipGetErrorString(e));
+  if (head_dim == 64 || head_dim == 128) {
+    if (dif::attention_split_bytes(head_dim) > bytes)
+      return fail(DIF_E_WORKSPACE, "static split workspace %zu bytes < required %zu", bytes,
+                  dif::attention_split_bytes(head_dim));
+  }
+  return attention_call(dtype, head_dim, flags, Q, ldq, K, ldk, Vt, ldvt, O, ldo, B, Lq, Lk,
+                        n_heads, part, bytes, stream);
+  GUARD_END
+}
+
 dif_status dif_profile_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   g_prof.on = on != 0;

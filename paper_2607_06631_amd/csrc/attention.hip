@@ -29,6 +29,7 @@
 // are ready the one issuing MFMAs wins and the other's softmax VALU work
 // fills the gaps (measured +2%).
 // The kernel fits in 256 registers per lane (two waves per SIMD).
+#include <mutex>
 #include <type_traits>
 
 #include "common.h"
@@ -478,6 +479,35 @@ void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream, int nc
 
 size_t attention_split_bytes(int head_dim) {
   return (size_t)2 * kMaxSplitItems * 256 * (head_dim + 2) * sizeof(float);
+}
+
+// Key-split partial sums for callers that cannot allocate: one buffer in
+// static device memory, which every device the library runs on holds until
+// the process ends.  Sized for head_dim 128 (the largest split workspace;
+// it does not grow with the problem, the split is capped at kMaxSplitItems
+// items).  Host code reaches it only through the address
+// hipGetSymbolAddress returns on each device.
+constexpr size_t kStaticSplitBytes = (size_t)2 * kMaxSplitItems * 256 * (128 + 2) * sizeof(float);
+static __device__ __align__(256) float scratch[kStaticSplitBytes / sizeof(float)];
+
+hipError_t attention_static_scratch(float** out, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static float* ptrs[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    ptrs[dev] = static_cast<float*>(p);
+  }
+  *out = ptrs[dev];
+  *bytes = kStaticSplitBytes;
+  return hipSuccess;
 }
 
 template <typename T>

@@ -57,6 +57,9 @@ hipError_t launch_attention(int head_dim, const T* Q, int64_t ldq, const T* K, i
                             int H, hipStream_t stream, bool q_scaled = false,
                             float* split_part = nullptr, int ncu = 0);
 size_t attention_split_bytes(int head_dim);
+// The library's static split workspace on the current device (resolved once
+// per device): its device address and size.
+hipError_t attention_static_scratch(float** ptr, size_t* bytes);
 constexpr int kAttnLongKeys = 4096;   // from this key count on, bf16 attention runs 8 waves
 
 // Row LayerNorm of x [M, D] then

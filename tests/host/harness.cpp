@@ -365,6 +365,10 @@ void operator_cases(Arena& ar) {
                           part, sb - 1, nullptr) == DIF_E_WORKSPACE);
   EXPECT(dif_attention_ex(DIF_BF16, dh, 0, Q, H * dh, K, H * dh, Vt, 320, O, H * dh, Bn, L, L, H,
                           (char*)part + 128, sb, nullptr) == DIF_E_WORKSPACE);
+  EXPECT(dif_attention_ex_static(DIF_BF16, dh, DIF_ATTN_Q_PRESCALED, Q, H * dh, K, H * dh, Vt, 320,
+                                 O, H * dh, Bn, L, L, H, nullptr) == DIF_OK);
+  EXPECT(dif_attention_ex_static(DIF_BF16, 96, 0, Q, H * dh, K, H * dh, Vt, 320, O, H * dh, Bn, L, L,
+                                 H, nullptr) == DIF_E_UNSUPPORTED);
   EXPECT(dif_attention(DIF_BF16, dh, Q, H * dh, K, H * dh, Vt, 200, O, H * dh, Bn, L, L, H, nullptr) ==
          DIF_E_SHAPE);
   EXPECT(dif_attention(DIF_BF16, dh, Q, H * dh, K, H * dh, Vt, 320, O, H * dh, Bn, L, 0, H, nullptr) ==

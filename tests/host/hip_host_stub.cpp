@@ -204,6 +204,13 @@ size_t attention_split_bytes(int head_dim) {
   return (size_t)2 * 128 * 256 * (head_dim + 2) * sizeof(float);
 }
 
+hipError_t attention_static_scratch(float** ptr, size_t* bytes) {
+  alignas(256) static float buf[2 * 128 * 256 * 130];
+  *ptr = buf;
+  *bytes = sizeof(buf);
+  return hipSuccess;
+}
+
 template <typename T>
 hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0, const float* p1,
                        const float* p2, const float* p3, float, hipStream_t) {
