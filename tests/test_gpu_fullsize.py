@@ -52,7 +52,12 @@ def _run(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="com
     return one, m1, x, ctx, e0, got
 
 
-def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="compact"):
+def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="compact",
+           update_check=False):
+    """Block output on sampled rows against the oracle: max |g - r| / max |r|
+    over the output x_out (asserted), and the same error relative to the
+    block's update x_out - x_in (printed; asserted with update_check, for
+    inputs built so that the update is the self-attention branch)."""
     one, m1, x, ctx, e0, got = _run(cfg, wl, masks, layer, seed, x_scale, gate_ffn_off, kind)
     say(f"  GPU block done ({kind} plan); oracle on sampled rows")
     rows = _rows(one.seq_len, seed)
@@ -61,8 +66,12 @@ def _check(cfg, wl, masks, layer, seed, x_scale=0.5, gate_ffn_off=False, kind="c
     ref = O.block(x[0], ctx[0], e0, wz, True, one.n_heads, one.head_dim, one.grid, one.rope_theta,
                   one.eps, rows=rows, dtype=np.float32)
     err = rel_err(got[rows], ref)
-    say(f"  rel err {err:.3e} over {len(rows)} rows")
+    x_in = x[0][rows].astype(np.float64)
+    err_upd = rel_err(got[rows] - x_in, ref - x_in)
+    say(f"  rel err {err:.3e} (update-relative {err_upd:.3e}) over {len(rows)} rows")
     assert err <= TOL
+    if update_check:
+        assert err_upd <= TOL
 
 
 @pytest.fixture(scope="module")
@@ -119,3 +128,53 @@ def test_wan14b_480p_indexed_equals_compact():
     got_i = _run(cfg, wl, masks, layer, seed=71, kind="indexed")[-1]
     got_c = _run(cfg, wl, masks, layer, seed=71, kind="compact")[-1]
     assert np.array_equal(got_i, got_c)
+
+
+# Self-attention-dominated blocks at full length: QK-norm gains x2 (sharp
+# scores), every cross-attention head pruned and the FFN gate at zero, so the
+# block's update is gate1 * (self-attention output Wo^T + bo) plus the
+# cross-attention output bias.  An odd number of kept heads at 32760 tokens
+# leaves the last round of attention workgroups half full, so this runs the
+# key split and merge as well.  The update is checked against the oracle's
+# update; the bf16 storage floor of these inputs (tests/bf16_emulation.py,
+# on CPU) is 1.3e-2 (Wan-1.3B width) and 1.1e-2 (Wan-14B width), and a
+# uniform self-attention would move the update by 0.9 and 1.0.
+
+@pytest.mark.parametrize("name,heads,seed", [("wan1.3b_block", 9, 90), ("wan14b_block", 29, 91)])
+def test_block_fullsize_self_attention_dominates(name, heads, seed):
+    cfg = get_config(name)
+    wl = synth.make_layer_weights(cfg, 0, 0, qk_gain=2.0)
+    f = cfg.keep_ffn[-1]
+    masks = synth.masks_from_counts(cfg, [heads], [0], [f])
+    _check(cfg, wl, masks, 0, seed=seed, gate_ffn_off=True, update_check=True)
+
+
+def test_wan14b_480p_step_with_every_block_gated_off():
+    """dif_step_forward at the benchmark's width and length with every block
+    gate 0: timestep embedding (e for the head modulation), the cast and
+    patch embedding of the latents, the output head's LayerNorm, modulation
+    and projection, against the oracle's step on sampled rows."""
+    import torch
+    cfg = get_config("wan14b_480p").with_(n_layers=1, name="wan14b_480p_head")
+    w = synth.make_global_weights(cfg, 0)
+    w["layers"] = [synth.make_layer_weights(get_config("wan14b_block"), 0, 0)]
+    model = make_model(cfg, w)
+    masks = synth.make_masks(get_config("wan14b_block"), 1)
+    masks["block_keep"][:] = 0
+    t = cfg.timesteps[1]
+    say(f"wan14b-width step, every block off: L={cfg.seq_len} t={t}")
+    plan = B.dif_plan_step(model, 1, t, masks)
+    z0 = synth.make_latents(cfg, seed=7)
+    ctx = synth.make_context(cfg, seed=7)
+    z = to_dev(z0, dtype=torch.float32)
+    v = torch.empty_like(z)
+    ws = B.workspace(model, 1, cfg.seq_len, cfg.text_len)
+    B.dif_step_forward(plan, z, t, to_dev(ctx, cfg), v, ws)
+    torch.cuda.synchronize()
+    rows = _rows(cfg.seq_len, 7)
+    got = to_np(v)[0][rows]
+    zr = z0[:, rows]
+    ref = O.step(zr, t, ctx, w, masks, cfg.with_(grid=(1, 1, len(rows))), dtype=np.float64)[0]
+    err = rel_err(got, ref)
+    say(f"  rel err {err:.3e} over {len(rows)} rows")
+    assert err <= TOL

@@ -8,9 +8,16 @@ block's input -- the GPU's own residual stream after the layers before it --
 goes to the oracle, which computes that block for sampled query rows (keys
 and values over all L tokens) with the keep masks applied by zeroing dense
 weights, and the GPU's block output must match within the bf16 tolerance.
-The modulation e0 is the library's own time embedding of t_s (its parity is
-checked at float32 on the tiny stack).  The oracle runs in float32 here to
-keep the masked-dense projections within seconds.
+The modulation e0 both sides use is the oracle's time embedding of t_s,
+computed in float64 from the stack's weights; the library's own embedding
+(dif_time_embed) is checked against it at the full width first.  The oracle
+runs in float32 here to keep the masked-dense projections within seconds.
+Besides the error relative to the block output, the error relative to the
+block's update x_out - x_in is printed; deep in the stack the residual
+stream is several times larger than one block's update, so its bf16
+storage alone (about 2^-9 of |x| per store, three stores per block) is a
+larger share of the update than the 2e-2 tolerance allows, and that
+figure is reported, not asserted.
 """
 import numpy as np
 import pytest
@@ -59,8 +66,15 @@ def test_wan14b_480p_stack_teacher_forced(stack, step):
     ctx = torch.randn((1, Lc, D), generator=gen, device="cuda").to(torch.bfloat16)
     ws = B.workspace(model, 1, L, Lc)
     e = torch.empty(D, device="cuda")
-    e0 = torch.empty(6 * D, device="cuda")
-    B.dif_time_embed(model, cfg.timesteps[step], e, e0, ws)
+    e0_lib = torch.empty(6 * D, device="cuda")
+    B.dif_time_embed(model, cfg.timesteps[step], e, e0_lib, ws)
+    wg = {k: w[k].float().cpu().numpy() for k in ("t_w1", "t_b1", "t_w2", "t_b2", "t_w3", "t_b3")}
+    e_ref, e0_ref = O.time_embedding(wg, cfg.timesteps[step])
+    torch.cuda.synchronize()
+    err_e = max(rel_err(to_np(e), e_ref), rel_err(to_np(e0_lib).reshape(6, D), e0_ref))
+    say(f"step {step}: time embedding at D={D}: rel err {err_e:.3e}")
+    assert err_e <= TOL
+    e0 = torch.from_numpy(e0_ref.astype(np.float32).reshape(-1)).cuda()
     # the residual stream entering layer 0: patch embedding of the latents
     x = (z.to(torch.bfloat16).float() @ w["patch_w"].float().t() + w["patch_b"])
     x = x.to(torch.bfloat16).reshape(1, L, D).contiguous()
@@ -84,6 +98,10 @@ def test_wan14b_480p_stack_teacher_forced(stack, step):
         ref = O.block(x_in, ctx_np, e0_np, wz, bool(masks["block_keep"][layer]), cfg.n_heads,
                       cfg.head_dim, cfg.grid, cfg.rope_theta, cfg.eps, rows=rows, dtype=np.float32)
         err = rel_err(x_out[rows], ref)
+        xi = x_in[rows].astype(np.float64)
+        err_upd = rel_err(x_out[rows] - xi, ref - xi)
         say(f"  layer {layer}: {int(masks['self_head_keep'][layer].sum())} heads, "
-            f"{int(masks['ffn_keep'][layer].sum())} channels: rel err {err:.3e} over {len(rows)} rows")
+            f"{int(masks['ffn_keep'][layer].sum())} channels: rel err {err:.3e} "
+            f"(update-relative {err_upd:.3e}, max|x| {np.abs(ref).max():.2f}, "
+            f"max|update| {np.abs(ref - xi).max():.2f}) over {len(rows)} rows")
         assert err <= TOL
