@@ -42,9 +42,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "5ff35620f3e58b3ef6a133ca24869fe563c1761883c91083d417195d0e4a6dc7",
-    "fetch_bytes": 1122453.0 * 1024 / 0.500,
-    "write_bytes": 429584.5 * 1024 / 1.000,
+    "sha256": "9993be05f09e45b53e70d432abc2538e5dcf5987a16fcfa768448d2011342106",
+    "fetch_bytes": 1106773.035546875 * 1024 / 0.500,
+    "write_bytes": 360503.526953125 * 1024 / 1.000,
 }
 
 
