@@ -299,3 +299,46 @@ def test_step_rejects_a_timestep_other_than_the_plans(tiny_model):
     free = B.dif_plan_step(model, 1, float("nan"), masks, any_t=True)
     B.dif_step_forward(free, z, cfg.timesteps[2], ctx, v, ws)
     torch.cuda.synchronize()
+
+
+def test_single_token_grid_step():
+    """The degenerate grid 1 x 1 x 1: one video token (attention over one
+    key returns its value) and one text token, through dif_step_forward, at
+    float32 against the oracle's step."""
+    import torch
+    cfg = TINY.with_(name="one_token", grid=(1, 1, 1), text_len=1)
+    say("single-token grid step")
+    w = synth.make_weights(cfg, seed=5, qk_gain=2.0)
+    model = make_model(cfg, w)
+    masks = synth.make_masks(cfg, 2)
+    plan = B.dif_plan_step(model, 2, cfg.timesteps[2], masks)
+    z0 = synth.make_latents(cfg, seed=5)
+    ctx = synth.make_context(cfg, seed=5)
+    z = to_dev(z0, dtype=torch.float32)
+    v = torch.empty_like(z)
+    ws = B.workspace(model, 1, 1, 1)
+    B.dif_step_forward(plan, z, cfg.timesteps[2], to_dev(ctx, cfg), v, ws)
+    torch.cuda.synchronize()
+    ref = O.step(z0, cfg.timesteps[2], ctx, w, masks, cfg)
+    err = rel_err(to_np(v), ref)
+    say(f"  rel err {err:.3e}")
+    assert err <= TOL["f32"]
+
+
+def test_widest_bf16_block():
+    """dim 8192 (64 heads of 128), the widest model the library accepts in
+    bfloat16, on a small ragged grid: a pruned block against the oracle."""
+    cfg = get_config("wan14b_block").with_(name="wide8192", dim=8192, n_heads=64, ffn_dim=2048,
+                                           grid=(1, 5, 7), text_len=9,
+                                           keep_heads=(47,), keep_ffn=(1384,), ffn_chunk=1)
+    say(f"dim-8192 block L={cfg.seq_len}")
+    w = synth.make_weights(cfg, seed=6)
+    model = make_model(cfg, w)
+    masks = synth.make_masks(cfg, 0)
+    x, ctx, e0 = _inputs(cfg, 6)
+    got, plan = gpu_block(model, cfg, masks, 0, 0, x, ctx, e0)
+    assert plan.layer_info(0).self_heads == 47
+    ref = oracle_block(cfg, w["layers"][0], masks, 0, x, ctx, e0)
+    err = rel_err(got, ref)
+    say(f"  rel err {err:.3e}")
+    assert err <= TOL["bf16"]
