@@ -294,12 +294,14 @@ def run_blocks(args, cfg):
         torch.cuda.synchronize()
         ms, _, prof = timed(B, run, args.steps, 0, not args.no_kernel_timing)
         ms_clean, _, _ = timed(B, run, args.steps, 0, False)
-        copy_ms = 2.0 * x0.numel() * 2 / 5.0e12 * 1e3   # the input copy, ~5 TB/s (subtracted)
+        # the input copy each call makes, timed alone and subtracted
+        copy_ms = float(np.median(timed(B, lambda i: x.copy_(x0), args.steps, 0, False)[0]))
         med = float(np.median(ms_clean)) - copy_ms
         per[f"t{s + 1}"] = {
             "heads": info.self_heads, "ffn_channels": info.ffn_channels,
             "ms_per_block": round(med, 3),
             "ms_per_block_with_kernel_events": round(float(np.median(ms)) - copy_ms, 3),
+            "input_copy_ms_subtracted": round(copy_ms, 4),
             "kept_tflop": round(kept / 1e12, 3), "executed_tflop": round(execd / 1e12, 3),
             "tflops": round(kept / (med * 1e-3) / 1e12, 1),
             "frac_peak": round(kept / (med * 1e-3) / 1e12 / peak, 4),
