@@ -305,7 +305,6 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
       u32x4 pc[NPC];
       float lh = 0.f;
       auto probs = [&]() {
-        lh = 0.f;
 #pragma unroll
         for (int u = 0; u < NPC; ++u) {
           float pv[VEC];
@@ -319,7 +318,7 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
           for (int w = VEC / 2; w > 0; w /= 2)
 #pragma unroll
             for (int e = 0; e < w; ++e) t[e] += t[e + w];
-          lh += t[0];
+          lh = u == 0 ? t[0] : lh + t[0];
         }
       };
       probs();

@@ -31,6 +31,27 @@
 #include "kernels.h"
 
 namespace dif {
+// Fragment k of a k-step in the order its MFMAs first use them (MFMA i
+// multiplies A row block i / TN by B column block i % TN): the value is a
+// row block index (< TM) or TM + a column block index.  For 4 x 2 blocks:
+// A0 B0 B1 A1 A2 A3.
+template <int TM, int TN>
+__device__ constexpr int first_use(int k) {
+  bool seen[TM + TN] = {};
+  int n = 0;
+  for (int i = 0; i < TM * TN; ++i) {
+    const int a = i / TN, b = TM + i % TN;
+    if (!seen[a]) {
+      seen[a] = true;
+      if (n++ == k) return a;
+    }
+    if (!seen[b]) {
+      seen[b] = true;
+      if (n++ == k) return b;
+    }
+  }
+  return k;
+}
 
 constexpr int G_BKC = 8;    // 16-byte chunks per k-tile row (128 bytes)
 constexpr int BN_MAX = 256; // largest workgroup tile width over the shapes below
@@ -99,9 +120,15 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   constexpr int VEC = Chunk<T>::VEC;
   constexpr int BK = BKC * VEC;
   constexpr int RPI = 64 / BKC;           // rows filled by one wave load instruction (1 KB)
-  constexpr int LA = BM / (RPI * NW), LB = BN / (RPI * NW);
+  // Eight waves: waves 0..3, the older wave of each SIMD pair, issue all of
+  // a tile's loads.  The older wave wins the SIMD's issue arbitration and
+  // finishes its share of a k-tile first; the loads' issue time then comes
+  // off the younger wave, which ends each k-tile (measured 4.7% on the
+  // step's five projection shapes).
+  constexpr int NLW = NW == 8 ? 4 : NW;   // loading waves
+  constexpr int LA = BM / (RPI * NLW), LB = BN / (RPI * NLW);
   constexpr int LPT = LA + LB;            // loads per thread per k-tile
-  static_assert(LA * RPI * NW == BM && LB * RPI * NW == BN, "staging split");
+  static_assert(LA * RPI * NLW == BM && LB * RPI * NLW == BN, "staging split");
   __shared__ u32x4 smem[2][BM + BN][BKC];
   static_assert(sizeof(smem) >= (size_t)NW * 64 * 64 * sizeof(float), "epilogue staging");
   extern __shared__ uint32_t kch_lds[];   // GA_KCH: byte offset of each K chunk
@@ -143,13 +170,16 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   const __amdgpu_buffer_rsrc_t b_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(b_base), (short)0, b_bytes, kRsrcWord3);
   uint32_t a_off[LA], b_off[LB];
-  // direct-to-LDS: instruction i of this wave fills LDS rows (i*NW + wave)*RPI
-  // .. +RPI (1 KB); lane l writes 16 bytes at 16*l, i.e. row +l/BKC, physical
-  // chunk l%BKC, and fetches the logical chunk the swizzle places there.
-  // The swizzle depends on row bits 0..3 only, which are l/BKC's (RPI = 16)
-  // or l/BKC's and the wave's parity (RPI = 8): one logical chunk for all i.
-  static_assert(RPI == 16 || (RPI == 8 && NW % 2 == 0), "direct staging layout");
-  auto drow = [&](int i) { return (i * NW + wave) * RPI + lane / BKC; };
+  // direct-to-LDS: instruction i of loading wave lw fills LDS rows
+  // (i*NLW + lw)*RPI .. +RPI (1 KB); lane l writes 16 bytes at 16*l, i.e. row
+  // +l/BKC, physical chunk l%BKC, and fetches the logical chunk the swizzle
+  // places there.  The swizzle depends on row bits 0..3 only, which are
+  // l/BKC's (RPI = 16) or l/BKC's and lw's parity (RPI = 8): one logical
+  // chunk for all i.
+  static_assert(RPI == 16 || (RPI == 8 && NLW % 2 == 0), "direct staging layout");
+  const int lw = wave % NLW;
+  const bool loader = wave < NLW;
+  auto drow = [&](int i) { return (i * NLW + lw) * RPI + lane / BKC; };
   const int dchunk = swz<BKC>(drow(0), lane % BKC);
 #pragma unroll
   for (int i = 0; i < LA; ++i)
@@ -182,17 +212,19 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
     }
   };
   typedef __attribute__((address_space(3))) void lds_t;
-  // load u (0 .. LPT-1) of this thread's share of tile kt: A rows, then B rows
-  auto issue_one = [&](int kt, int u) {
+  // load u (0 .. LPT-1) of this loading wave's share of tile kt into stage
+  // st: A rows, then B rows (LDS destinations from a scalar wave index)
+  const int lw_s = __builtin_amdgcn_readfirstlane(lw);
+  auto issue_one = [&](int kt, int u, auto st_c) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    const int st = kt & 1;
+    constexpr int st = decltype(st_c)::value;
     const int koff = kt * BK * (int)sizeof(T);
     if (u < LA) {
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, (lds_t*)&smem[st][(u * NW + wave) * RPI][0],
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, (lds_t*)&smem[st][(u * NLW + lw_s) * RPI][0],
                                                16, a_off[u], koff, 0, 0);
     } else {
       const int i = u - LA;
-      lds_t* dst = (lds_t*)&smem[st][BM + (i * NW + wave) * RPI][0];
+      lds_t* dst = (lds_t*)&smem[st][BM + (i * NLW + lw_s) * RPI][0];
       if constexpr (GA == GA_KCH)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b_off[i] + kb, 0, 0, 0);
       else
@@ -202,7 +234,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   };
   auto issue = [&](int kt) {
 #pragma unroll
-    for (int u = 0; u < LPT; ++u) issue_one(kt, u);
+    for (int u = 0; u < LPT; ++u)
+      if (loader) issue_one(kt, u, std::integral_constant<int, 0>{});
   };
 
   f32x16 acc[TM][TN];
@@ -213,60 +246,67 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // MFMA operand fragments, double-buffered in registers: each k-step's
-  // fragments are read from LDS before the previous k-step's MFMAs are
-  // issued.  Scheduling barriers keep that order (left alone, the compiler
-  // sinks every read next to its first use).
+  // MFMA operand fragments, double-buffered in registers: the fragments of
+  // k-step ks+1 are read while the MFMAs of k-step ks issue, one read after
+  // each MFMA, in the order k-step ks+1's MFMAs first use them.  Scheduling
+  // barriers keep that order (left alone, the compiler sinks every read next
+  // to its first use).
   constexpr int KSN = BKC / 2;   // MFMA k-steps per k-tile
   static_assert(KSN % 2 == 0, "fragment slots alternate");
   u32x4 fa[2][TM], fb[2][TN];
-  auto frag = [&](int st, int ks, int slot) {
+  // fragment read r (first_use order) of k-step ks of stage st into slot
+  auto frag_one = [&](int st, int ks, int slot, int r) {
     const int c = swz<BKC>(col, 2 * ks + g);   // rows are col + multiples of 32
-#pragma unroll
-    for (int i = 0; i < TM; ++i) fa[slot][i] = smem[st][wm * TM * 32 + i * 32 + col][c];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) fb[slot][j] = smem[st][BM + wn * TN * 32 + j * 32 + col][c];
+    if (r < TM) fa[slot][r] = smem[st][wm * TM * 32 + r * 32 + col][c];
+    else fb[slot][r - TM] = smem[st][BM + wn * TN * 32 + (r - TM) * 32 + col][c];
   };
-  auto mma = [&](int slot) {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j) Mma<T>::step(acc[i][j], fa[slot][i], fb[slot][j]);
-  };
-  // one k-tile: wait for this wave's loads of tile kt, barrier (everyone's
-  // have landed and everyone is done with tile kt-1's stage), compute tile
-  // kt while requesting tile kt+1 into that stage.  Half of a wave's loads
-  // go out before the first k-step and half after its MFMAs: issued in one
-  // burst, the loads of all eight waves block the in-order issue of both
-  // waves of a SIMD at once (measured: ~5% slower on the step's shapes).
+  // One k-tile (stage st is compile-time, so fragment and load addresses are
+  // constants plus immediate offsets): wait for this wave's loads of tile kt,
+  // barrier (everyone's have landed and everyone is done with tile kt-1's
+  // stage), compute tile kt while requesting tile kt+1 into that stage.  Half
+  // of the loads go out before the first k-step and half after its MFMAs:
+  // issued in one burst, or spread over the k-steps, they measured slower.
   if (nk > 0) {
     kb_fetch(0);
     issue(0);
     kb_fetch(1);
   }
-  for (int kt = 0; kt < nk; ++kt) {
-    const int st = kt & 1;
+  auto ktile = [&](int kt, auto st_c) {
+    constexpr int st = decltype(st_c)::value;
+    using NS = std::integral_constant<int, st ^ 1>;
     const bool more = kt + 1 < nk;
     wait_vmcnt<0>();
     __syncthreads();
-    if (more) {
+    if (more && loader) {
 #pragma unroll
-      for (int u = 0; u < LPT / 2; ++u) issue_one(kt + 1, u);
+      for (int u = 0; u < LPT / 2; ++u) issue_one(kt + 1, u, NS{});
     }
-    frag(st, 0, 0);
+#pragma unroll
+    for (int r = 0; r < TM + TN; ++r) frag_one(st, 0, 0, first_use<TM, TN>(r));
 #pragma unroll
     for (int ks = 0; ks < KSN; ++ks) {
-      if (ks + 1 < KSN) frag(st, ks + 1, (ks + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
-      mma(ks & 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (ks == 0 && more) {
 #pragma unroll
-        for (int u = LPT / 2; u < LPT; ++u) issue_one(kt + 1, u);
+      for (int i = 0; i < TM * TN; ++i) {
+        Mma<T>::step(acc[i / TN][i % TN], fa[ks & 1][i / TN], fb[ks & 1][i % TN]);
+        if (ks + 1 < KSN && i < TM + TN) frag_one(st, ks + 1, (ks + 1) & 1, first_use<TM, TN>(i));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      if (ks == 0 && more && loader) {
+#pragma unroll
+        for (int u = LPT / 2; u < LPT; ++u) issue_one(kt + 1, u, NS{});
       }
       __builtin_amdgcn_sched_barrier(0);
     }
     kb_fetch(kt + 2);
+  };
+  {
+    int kt = 0;
+    for (; kt + 2 <= nk; kt += 2) {
+      ktile(kt, std::integral_constant<int, 0>{});
+      ktile(kt + 1, std::integral_constant<int, 1>{});
+    }
+    if (kt < nk) ktile(kt, std::integral_constant<int, 0>{});
   }
   __syncthreads();
 
