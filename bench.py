@@ -42,9 +42,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "9993be05f09e45b53e70d432abc2538e5dcf5987a16fcfa768448d2011342106",
-    "fetch_bytes": 1106773.035546875 * 1024 / 0.500,
-    "write_bytes": 360503.526953125 * 1024 / 1.000,
+    "sha256": "ee9eaaa578585787afb49ad99150ea906a78bfc3758fc7f0a53c9bc36a35d09b",
+    "fetch_bytes": 1107788.9640625 * 1024 / 0.500,
+    "write_bytes": 355332.070703125 * 1024 / 1.000,
 }
 
 
