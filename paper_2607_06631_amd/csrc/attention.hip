@@ -1,9 +1,16 @@
 // Bidirectional flash attention on MFMA for gfx950.
 //
-// Work split: one workgroup = 8 waves of one (sample, head); a wave owns 32
-// queries and walks all keys in tiles of 64, as two 32-key halves.  Eight
-// waves share each K / V^T tile copied into LDS, which halves those copies
-// per flop against four waves (measured +4%); one workgroup fills a CU.
+// Three kernels share one arithmetic: bf16 with head_dim 128 on long key
+// sequences (the blocks' self-attention) runs flash_attn_g2_kernel, four
+// waves of two 32-query groups each (below); the other long-key cases run
+// the eight-wave flash_attn_kernel, short key sequences (text tokens) and
+// float32 the four-wave one.
+//
+// Work split of flash_attn_kernel: one workgroup = 8 waves of one (sample,
+// head); a wave owns 32 queries and walks all keys in tiles of 64, as two
+// 32-key halves.  Eight waves share each K / V^T tile copied into LDS,
+// which halves those copies per flop against four waves (measured +4%);
+// one workgroup fills a CU.
 //
 // The scores are computed transposed, S^T = K Q^T, with MFMA 32x32 tiles:
 // the A operand is the K tile (rows = keys, from LDS), the B operand is
@@ -42,6 +49,7 @@ namespace dif {
 // sequences (the text tokens), where eight waves leave too few workgroups and
 // too few key tiles to amortise each workgroup's prologue
 constexpr int kLongKeys = kAttnLongKeys;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int kMaxSplitItems = 128;   // split items one workspace region holds
 constexpr int AT_BN = 64;        // keys per tile
 constexpr float kSlack = 8.f;    // log2 headroom of the lazy softmax rescale
@@ -448,6 +456,599 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
   }
 }
 
+// Long bf16 key sequences, head_dim 128: two 32-query groups per wave.
+//
+// One workgroup = 4 waves, one per SIMD, each owning 64 queries as two
+// groups of 32 (g0, g1); 256 queries per workgroup as in the eight-wave
+// kernel.  Every K and V^T fragment read from LDS feeds the MFMAs of both
+// groups, so LDS fragment reads per flop are half the eight-wave kernel's.
+// The score, softmax and output arithmetic is the eight-wave kernel's, in
+// the same order per query (same K layout, transposed scores with -m in
+// the accumulator, the same lazy-rescale test on the same 32 queries), so
+// the two kernels give bit-identical results.
+//
+// With one wave per SIMD the wave hides its own softmax: the key loop is a
+// software pipeline of blocks of 16 MFMAs, each carrying the softmax of one
+// group's 32-key half:
+//   X(t,h): S(t,h,g1) = K Q1^T and O1 += V^T P(prev,g1);  softmax S(t,h,g0)
+//   Y(t,h): S(next,g0) = K Q0^T and O0 += V^T P(t,h,g0);  softmax S(t,h,g1)
+// Score and output MFMAs alternate, so no MFMA waits for the one before
+// it; after each MFMA come at most one LDS read, one exponential, one bf16
+// pack and two adds of the row sum.  K fragments of the next half are read
+// behind the score MFMAs that consume the current ones, V^T fragments
+// behind the output MFMAs, so every read has a block of MFMAs to land.
+//
+// K / V^T tiles sit in a ring of three LDS buffers with one workgroup
+// barrier per tile, after the first MFMA of X(t,1) (which reads no LDS):
+// it publishes tile t+1 (each wave waited for its own direct-to-LDS loads)
+// and frees the buffer of tile t-1, into which tile t+2 is then loaded,
+// one load instruction behind each score MFMA.  Each ring slot is its own
+// LDS variable, which is what lets the compiler see that those loads
+// cannot alias the reads of the other slots (otherwise it waits for them
+// before every read).  (A four-slot ring, two tiles in flight, measured
+// 0.4 % slower.)
+//
+// The MFMAs are inline assembly so that the Q^T fragments and the O^T
+// accumulators stay in AGPRs (the 512 registers of a lone wave hold both
+// groups only with them there) while scores and fragments stay in VGPRs.
+// The compiler does not see inline MFMAs as MFMAs, so the code keeps the
+// hardware's dependency distances itself: an MFMA result is read by the
+// VALU only after at least two further MFMAs and a dozen instructions, an
+// explicit wait precedes the first output MFMA of a block (two wait states
+// after the VALU writes its operand), and the rare rescale path and the
+// epilogue wait out the MFMA pipeline before touching the accumulators.
+// Measured against the eight-wave kernel on the blocks' launch (32760
+// tokens, 24-40 heads): +6.4 to +6.7 %.
+namespace g2 {
+__device__ __forceinline__ void mma_sc(f32x16& d, const u32x4& a, const u32x4& b, const f32x16& c) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+}
+__device__ __forceinline__ void mma_s(f32x16& d, const u32x4& a, const u32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
+}
+__device__ __forceinline__ void mma_o(f32x16& d, const u32x4& a, const u32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(d) : "v"(a), "v"(b));
+}
+__device__ __forceinline__ void mma_o_first(f32x16& d, const u32x4& a, const u32x4& b) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(d) : "v"(a), "v"(b));
+}
+// wait out the MFMA pipeline before the VALU reads an MFMA result
+__device__ __forceinline__ void mfma_drain() { asm volatile("s_nop 15\n\ts_nop 15" ::); }
+// two wait states after the VALU wrote an MFMA operand
+__device__ __forceinline__ void valu_to_mfma() { asm volatile("s_nop 4" ::); }
+template <typename X>
+__device__ __forceinline__ void pin(X& x) { asm volatile("" : "+v"(x)); }
+template <typename X>
+__device__ __forceinline__ void pin_a(X& x) { asm volatile("" : "+a"(x)); }
+// a volatile LDS read, kept in program order among the inline MFMAs
+__device__ __forceinline__ u32x4 lds_read(const u32x4* ptr) {
+  typedef __attribute__((address_space(3))) const volatile u32x4 lds_u32x4;
+  return *(lds_u32x4*)ptr;
+}
+}  // namespace g2
+
+template <bool SC>
+__global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> p) {
+  using T = bf16;
+  constexpr int NBUF = 3;   // LDS ring slots
+  constexpr int DH = 128, W = 4, THREADS = 256, VEC = 8;
+  constexpr int KCH = DH * 2 / 16;       // 16 chunks per K row
+  constexpr int VCH = AT_BN * 2 / 16;    // 8 chunks per V^T row
+  constexpr int NQS = DH / 16;           // 8 MMA steps over head_dim
+  constexpr int BMQ = 256;
+  constexpr int K_PER_T = AT_BN * KCH / THREADS;
+  constexpr int V_PER_T = DH * VCH / THREADS;
+  static_assert(K_PER_T * THREADS == AT_BN * KCH && V_PER_T * THREADS == DH * VCH, "tile split");
+  // one LDS variable per ring slot: the compiler tells direct-to-LDS loads
+  // into one slot from reads of another only across distinct variables
+  __shared__ u32x4 ks0_[AT_BN][KCH], ks1_[AT_BN][KCH], ks2_[AT_BN][KCH];
+  __shared__ u32x4 vs0_[DH][VCH], vs1_[DH][VCH], vs2_[DH][VCH];
+  auto kbuf = [&](int b) __attribute__((always_inline)) -> u32x4(*)[KCH] {
+    return b == 0 ? ks0_ : b == 1 ? ks1_ : ks2_;
+  };
+  auto vbuf = [&](int b) __attribute__((always_inline)) -> u32x4(*)[VCH] {
+    return b == 0 ? vs0_ : b == 1 ? vs1_ : vs2_;
+  };
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = lane >> 5, col = lane & 31;
+
+  const int nqb = (p.Lq + BMQ - 1) / BMQ;
+  const int ntiles = (p.Lk + AT_BN - 1) / AT_BN;
+  int bid, split = -1, t0 = 0, t1 = ntiles;
+  if ((int)blockIdx.x < p.nreg) {
+    bid = xcd_remap(blockIdx.x, p.nreg);
+  } else {
+    const int sidx = (int)blockIdx.x - p.nreg;
+    bid = p.nreg + (sidx >> 1);
+    split = sidx;
+    if (sidx & 1) t0 = p.split_tile;
+    else t1 = p.split_tile;
+  }
+  const int qb = bid % nqb, hb = bid / nqb;
+  const int h = hb % p.H, b = hb / p.H;
+
+  u32x4 qf[2][NQS];
+#pragma unroll
+  for (int gr = 0; gr < 2; ++gr) {
+    const int q = qb * BMQ + wave * 64 + gr * 32 + col;
+    const int64_t qrow = (int64_t)b * p.Lq + min(q, p.Lq - 1);
+#pragma unroll
+    for (int s = 0; s < NQS; ++s)
+      qf[gr][s] = *reinterpret_cast<const u32x4*>(p.Q + qrow * p.ldq + h * DH + (2 * s + g) * VEC);
+  }
+#pragma unroll
+  for (int gr = 0; gr < 2; ++gr)
+#pragma unroll
+    for (int s = 0; s < NQS; ++s) g2::pin_a(qf[gr][s]);   // AGPRs from here on
+
+  const T* kbase = p.K + (int64_t)b * p.Lk * p.ldk + h * DH;
+  const T* vbase = p.Vt + ((int64_t)b * p.H + h) * DH * p.ldvt;
+
+  // direct-to-LDS tile copies, as in the eight-wave kernel
+  constexpr uint32_t kRsrcWord3 = 0x00020000u;
+  constexpr int ES = 2;
+  constexpr int KRPI = 64 / KCH;
+  constexpr int VRPI = 64 / VCH;
+  constexpr int KI = AT_BN / (KRPI * W);
+  constexpr int VI = DH / (VRPI * W);
+  static_assert(KI * KRPI * W == AT_BN && VI * VRPI * W == DH, "direct tile split");
+  uint32_t kd_off[KI], vd_off[VI];
+#pragma unroll
+  for (int j = 0; j < KI; ++j) {
+    const int row = (j * W + wave) * KRPI + lane / KCH;
+    const int kk = row >> 5, i = row & 31;
+    const int key = kk * 32 + 16 * ((i >> 2) & 1) + 4 * (i >> 3) + (i & 3);
+    kd_off[j] = (uint32_t)((key * p.ldk + swz<KCH>(row, lane % KCH) * VEC) * ES);
+  }
+#pragma unroll
+  for (int j = 0; j < VI; ++j) {
+    const int d = (j * W + wave) * VRPI + lane / VCH;
+    vd_off[j] = (uint32_t)((d * p.ldvt + swz<VCH>(d, lane % VCH) * VEC) * ES);
+  }
+  const int64_t v_bytes = (int64_t)DH * p.ldvt * ES;
+  auto k_rsrc = [&](int key0) {
+    const int64_t kb = (int64_t)(p.Lk - key0) * p.ldk * ES;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(kbase + (int64_t)key0 * p.ldk), (short)0,
+                                             (uint32_t)(kb < 0xffffffffll ? kb : 0xffffffffll),
+                                             kRsrcWord3);
+  };
+  auto load_direct = [&](int kt, auto buf_c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int buf = (int)buf_c;
+    typedef __attribute__((address_space(3))) void lds_t;
+    const int key0 = kt * AT_BN;
+    const __amdgpu_buffer_rsrc_t kr = k_rsrc(key0);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
+#pragma unroll
+    for (int j = 0; j < KI; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_t*)&kbuf(buf)[(j * W + wave) * KRPI][0], 16,
+                                               kd_off[j], 0, 0, 0);
+#pragma unroll
+    for (int j = 0; j < VI; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vbuf(buf)[(j * W + wave) * VRPI][0], 16,
+                                               vd_off[j], 0, 0, 0);
+#endif
+  };
+  // one direct-to-LDS instruction j of tile kt (j < KI: K rows, else V^T
+  // rows), LDS address from the wave index in an SGPR
+  [[maybe_unused]] const int wave_s = __builtin_amdgcn_readfirstlane(wave) & (W - 1);   // (known range 0..W-1)
+  auto load_one = [&](int kt, int buf, int j) __attribute__((always_inline)) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    typedef __attribute__((address_space(3))) void lds_t;
+    const int key0 = kt * AT_BN;
+    if (j < KI) {
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(k_rsrc(key0), (lds_t*)&kbuf(buf)[(j * W + wave_s) * KRPI][0], 16,
+                                               kd_off[j], 0, 0, 0);
+    } else {
+      const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vbuf(buf)[((j - KI) * W + wave_s) * VRPI][0], 16,
+                                               vd_off[j - KI], 0, 0, 0);
+    }
+#endif
+  };
+  auto load_tail = [&](int kt, auto buf_c) {
+    const int buf = (int)buf_c;
+    const int key0 = kt * AT_BN;
+    const __amdgpu_buffer_rsrc_t kr = k_rsrc(key0);
+#pragma unroll
+    for (int i = 0; i < K_PER_T; ++i) {
+      const int id = tid + THREADS * i;
+      const int kl = id / KCH, c = id % KCH;
+      const u32x4 v = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(kr, (uint32_t)((kl * p.ldk + c * VEC) * ES), 0, 0));
+      const int row = (kl & ~31) + key_slot(kl & 31);
+      kbuf(buf)[row][swz<KCH>(row, c)] = v;
+    }
+#pragma unroll
+    for (int i = 0; i < V_PER_T; ++i) {
+      const int id = tid + THREADS * i;
+      const int d = id / VCH, c = id % VCH, k0 = key0 + c * VEC;
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (k0 < p.Lk) {
+        float tmp[VEC];
+        Chunk<T>::unpack(*reinterpret_cast<const u32x4*>(vbase + (int64_t)d * p.ldvt + k0), tmp);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e)
+          if (k0 + e >= p.Lk) tmp[e] = 0.f;
+        v = Chunk<T>::pack(tmp);
+      }
+      vbuf(buf)[d][swz<VCH>(d, c)] = v;
+    }
+  };
+  auto load_tile = [&](int kt, auto buf_c) {
+    if ((kt + 1) * AT_BN <= p.Lk) load_direct(kt, buf_c);
+    else load_tail(kt, buf_c);
+  };
+
+  f32x16 o[2][DH / 32];
+#pragma unroll
+  for (int gr = 0; gr < 2; ++gr)
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[gr][dt][r] = 0.f;
+#pragma unroll
+  for (int gr = 0; gr < 2; ++gr)
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt) g2::pin_a(o[gr][dt]);
+  float l_run[2] = {0.f, 0.f}, m_run[2];
+  f32x16 negm[2], s[2];
+  u32x4 kf[NQS], vf[8];
+  u32x4 pc[2][2];
+  const float uscale = SC ? 1.f : p.c;
+
+  // (buf: a compile-time buffer, or a run-time one for the last tile)
+  auto read_k = [&](auto buf_c, int kk, int i) __attribute__((always_inline)) {
+    const int buf = (int)buf_c;
+    kf[i] = g2::lds_read(&kbuf(buf)[kk * 32 + col][swz<KCH>(col, 2 * i + g)]);
+  };
+  // fragment i = 4 u + dt: head dims [32 dt, 32 dt + 32), keys 8 u.. of the lane group's 16
+  auto read_v = [&](auto buf_c, int kk, int i) __attribute__((always_inline)) {
+    const int buf = (int)buf_c;
+    const int u = i >> 2, dt = i & 3;
+    vf[i] = g2::lds_read(&vbuf(buf)[dt * 32 + col][swz<VCH>(col, (kk * 32 + 16 * g) / VEC + u)]);
+  };
+  auto mask = [&](f32x16& x, int key) {   // keys >= Lk -> -inf
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if (key + 16 * g + r >= p.Lk) x[r] = -INFINITY;
+  };
+  // softmax pieces of group gr: exponential of score e, then per 8-key chunk
+  // u the packed P^T operand and the chunk's probability sum
+  float pe[2][16];
+  float lsum[2][2];
+  float ta[2][2][4], tb[2][2][2];   // the row-sum tree of each 8-key chunk
+  // Slot i of group gr's softmax, issued after one MFMA: the exponential of
+  // score i, the bf16 pair (i-1, i) of the P^T operand, and the adds of the
+  // chunk's sum tree ((e0+e4)+(e2+e6)) + ((e1+e5)+(e3+e7)) that have their
+  // inputs -- at most four VALU instructions between two MFMAs.
+  auto sm_slot = [&](int gr, int i) __attribute__((always_inline)) {
+    float x = s[gr][i];
+    if constexpr (!SC) x *= uscale;
+    pe[gr][i] = __builtin_amdgcn_exp2f(x);
+    g2::pin(pe[gr][i]);
+    const int u = i >> 3, k = i & 7;
+    if (i & 1) {
+      bf16x2 v2 = {(bf16)pe[gr][i - 1], (bf16)pe[gr][i]};
+      pc[gr][u][k >> 1] = __builtin_bit_cast(uint32_t, v2);
+      g2::pin(pc[gr][u]);
+    }
+    if (k >= 4) {
+      ta[gr][u][k - 4] = pe[gr][i - 4] + pe[gr][i];
+      g2::pin(ta[gr][u][k - 4]);
+    }
+    if (k == 6) {
+      tb[gr][u][0] = ta[gr][u][0] + ta[gr][u][2];
+      g2::pin(tb[gr][u][0]);
+    }
+    if (k == 7) {
+      tb[gr][u][1] = ta[gr][u][1] + ta[gr][u][3];
+      g2::pin(tb[gr][u][1]);
+    }
+    if (i == 8) {
+      lsum[gr][0] = tb[gr][0][0] + tb[gr][0][1];
+      g2::pin(lsum[gr][0]);
+    }
+  };
+  auto sm_end = [&](int gr) __attribute__((always_inline)) {
+    lsum[gr][1] = tb[gr][1][0] + tb[gr][1][1];
+  };
+  auto sm_exp = [&](int gr, int e) __attribute__((always_inline)) {
+    float x = s[gr][e];
+    if constexpr (!SC) x *= uscale;
+    pe[gr][e] = __builtin_amdgcn_exp2f(x);
+    g2::pin(pe[gr][e]);
+  };
+  auto sm_pack = [&](int gr, int u) __attribute__((always_inline)) {
+    pc[gr][u] = Chunk<T>::pack(&pe[gr][8 * u]);
+    float t[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) t[e] = pe[gr][8 * u + e];
+#pragma unroll
+    for (int w = VEC / 2; w > 0; w /= 2)
+#pragma unroll
+      for (int e = 0; e < w; ++e) t[e] += t[e + w];
+    lsum[gr][u] = t[0];
+    g2::pin(pc[gr][u]);
+    g2::pin(lsum[gr][u]);
+  };
+  // Lazy rescale of group gr after its half's probabilities (see the
+  // eight-wave kernel): rare; it reads and rewrites the AGPR accumulators.
+  auto sm_check = [&](int gr) __attribute__((always_inline)) {
+    float lh = lsum[gr][0] + lsum[gr][1];
+    if (__any(!(lh <= (float)(1 << (int)kSlack)))) {
+      g2::mfma_drain();
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[gr][r]);
+      const float d = fmaxf(fmaxf(mx, __shfl_xor(mx, 32)) * uscale, 0.f);
+      const float alpha = __builtin_amdgcn_exp2f(-d);
+      l_run[gr] *= alpha;
+      // one accumulator at a time (16 registers through the VALU)
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt) {
+        g2::pin_a(o[gr][dt]);   // its reads cannot move above this point
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[gr][dt][r] *= alpha;
+        g2::pin_a(o[gr][dt]);
+      }
+      const float dm = d / uscale;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        s[gr][r] -= dm;
+        negm[gr][r] -= dm;
+      }
+      m_run[gr] += d;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) sm_exp(gr, e);
+      sm_pack(gr, 0);
+      sm_pack(gr, 1);
+      lh = lsum[gr][0] + lsum[gr][1];
+      g2::valu_to_mfma();
+    }
+    l_run[gr] += lh;
+  };
+
+  // ---- prologue: tiles t0 .. t0+NBUF-2 in flight, the base m of each group
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  load_tile(t0, I0{});
+  load_tile(t0 + 1, I1{});
+  wait_vmcnt<0>();
+  __syncthreads();
+  {
+    f32x16 z;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[r] = 0.f;
+#pragma unroll
+    for (int i = 0; i < NQS; ++i) read_k(I0{}, 0, i);
+#pragma unroll
+    for (int gr = 0; gr < 2; ++gr) {
+      g2::mma_sc(s[gr], kf[0], qf[gr][0], z);
+#pragma unroll
+      for (int i = 1; i < NQS; ++i) g2::mma_s(s[gr], kf[i], qf[gr][i]);
+    }
+    g2::mfma_drain();
+#pragma unroll
+    for (int gr = 0; gr < 2; ++gr) {
+      if (t0 * AT_BN + 32 > p.Lk) mask(s[gr], t0 * AT_BN);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[gr][r]);
+      m_run[gr] = fmaxf(mx, __shfl_xor(mx, 32)) * uscale;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) negm[gr][r] = -m_run[gr] / uscale;
+    }
+    g2::valu_to_mfma();
+    // S(t0, 0, g0) against the base
+    g2::mma_sc(s[0], kf[0], qf[0][0], negm[0]);
+#pragma unroll
+    for (int i = 1; i < NQS; ++i) g2::mma_s(s[0], kf[i], qf[0][i]);
+  }
+
+  // X(t, H): S(t,H,g1), then O1 += V^T P(prev, g1); softmax of S(t,H,g0).
+  // NEXT: a next half exists (its K fragments are read here); FIRST: no
+  // previous half (t = t0, H = 0).
+  auto blockX = [&](int t, auto buf_c, auto h_c, auto next_c, auto first_c, auto masked_c) __attribute__((always_inline)) {
+    constexpr bool MASKED = decltype(masked_c)::value;
+    constexpr int H = decltype(h_c)::value;
+    constexpr bool NEXT = decltype(next_c)::value;
+    constexpr bool FIRST = decltype(first_c)::value;
+    const auto Bc = buf_c;
+    const int key0 = t * AT_BN + H * 32;
+    // H = 1 with a next tile: the tile barrier, then tile t+NBUF-1 is loaded
+    // into tile t-1's buffer.  With a compile-time buffer the eight loads go
+    // one behind each score MFMA, unconditionally: past the range (or for
+    // the key-tail tile, which is then rewritten through registers) they
+    // load the last full tile into the free buffer.
+    constexpr bool CT = !std::is_integral<decltype(buf_c)>::value;
+    constexpr bool LOADS = H == 1 && NEXT;
+    const int lt = t + NBUF - 1;
+    const int lbuf = ((int)buf_c + NBUF - 1) % NBUF;
+    const int nfull = p.Lk / AT_BN;
+    if constexpr (FIRST) {
+      // S(t0,0,g0) was just computed: wait out the MFMA pipeline
+      g2::mfma_drain();
+#pragma unroll
+      for (int i = 0; i < 8; ++i) read_v(Bc, H, i);
+    }
+    if constexpr (MASKED) {
+      if (key0 + 32 > p.Lk) mask(s[0], key0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    // score and output MFMAs alternate, so no MFMA waits on the one before it
+#pragma unroll
+    for (int i = 0; i < NQS; ++i) {
+      if (i == 0) g2::mma_sc(s[1], kf[0], qf[1][0], negm[1]);
+      else g2::mma_s(s[1], kf[i], qf[1][i]);
+      if constexpr (LOADS) {
+        if (i == 0) {
+          // (the first score MFMA reads no LDS and runs under the barrier)
+          // tile t+1 landed (own loads) and every read of tile t-1 done
+          __builtin_amdgcn_s_waitcnt(0 | (7 << 4) | (0 << 8));   // vmcnt(0) lgkmcnt(0)
+          asm volatile("" ::: "memory");
+          __builtin_amdgcn_s_barrier();
+          if constexpr (!CT) {
+            if (lt < t1) load_tile(lt, lbuf);
+          }
+        }
+      }
+      if constexpr (NEXT) {
+        if constexpr (H == 0) read_k(Bc, 1, i);
+        else read_k(((int)buf_c + 1) % NBUF, 0, i);   // tile t+1's buffer
+      }
+      if constexpr (LOADS && CT) load_one(min(lt, nfull - 1), lbuf, i);
+      sm_slot(0, 2 * i);
+      __builtin_amdgcn_sched_barrier(0);
+      if constexpr (!FIRST) {
+        if (i == 0) g2::mma_o_first(o[1][i & 3], vf[i], pc[1][i >> 2]);
+        else g2::mma_o(o[1][i & 3], vf[i], pc[1][i >> 2]);
+        read_v(Bc, H, i);
+      }
+      sm_slot(0, 2 * i + 1);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if constexpr (LOADS && CT) {
+      if (lt < t1 && (lt + 1) * AT_BN > p.Lk) {   // the key-tail tile, once
+        wait_vmcnt<0>();
+        load_tail(lt, lbuf);
+      }
+    }
+    // (without output MFMAs behind them, the scores of g1 need the drain)
+    if constexpr (FIRST) g2::mfma_drain();
+    sm_end(0);
+    sm_check(0);
+  };
+  // Y(t, H): S(next, g0), then O0 += V^T P(t,H,g0); softmax of S(t,H,g1).
+  auto blockY = [&](int t, auto buf_c, auto h_c, auto next_c, auto masked_c) __attribute__((always_inline)) {
+    constexpr bool MASKED = decltype(masked_c)::value;
+    constexpr bool NEXT = decltype(next_c)::value;
+    constexpr int H = decltype(h_c)::value;
+    const int key0 = t * AT_BN + H * 32;
+    if constexpr (MASKED) {
+      if (key0 + 32 > p.Lk) mask(s[1], key0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NEXT) {
+#pragma unroll
+      for (int i = 0; i < NQS; ++i) {
+        if (i == 0) g2::mma_sc(s[0], kf[0], qf[0][0], negm[0]);
+        else g2::mma_s(s[0], kf[i], qf[0][i]);
+        sm_slot(1, 2 * i);
+        __builtin_amdgcn_sched_barrier(0);
+        if (i == 0) g2::mma_o_first(o[0][i & 3], vf[i], pc[0][i >> 2]);
+        else g2::mma_o(o[0][i & 3], vf[i], pc[0][i >> 2]);
+        sm_slot(1, 2 * i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        if (i == 0) g2::mma_o_first(o[0][i & 3], vf[i], pc[0][i >> 2]);
+        else g2::mma_o(o[0][i & 3], vf[i], pc[0][i >> 2]);
+        sm_slot(1, 2 * i);
+        sm_slot(1, 2 * i + 1);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    sm_end(1);
+    sm_check(1);
+  };
+  using TF = std::true_type;
+  using FF = std::false_type;
+  auto tile = [&](int t, auto buf_c, auto last_c) __attribute__((always_inline)) {
+    constexpr bool LAST = decltype(last_c)::value;
+    // only the last tile of the range can end past Lk
+    blockX(t, buf_c, I0{}, TF{}, FF{}, last_c);
+    blockY(t, buf_c, I0{}, TF{}, last_c);
+    blockX(t, buf_c, I1{}, std::integral_constant<bool, !LAST>{}, FF{}, last_c);
+    blockY(t, buf_c, I1{}, std::integral_constant<bool, !LAST>{}, last_c);
+  };
+
+  // first tile (its first block has no previous half)
+  blockX(t0, I0{}, I0{}, TF{}, TF{}, FF{});
+  blockY(t0, I0{}, I0{}, TF{}, FF{});
+  blockX(t0, I0{}, I1{}, TF{}, FF{}, FF{});
+  blockY(t0, I0{}, I1{}, TF{}, FF{});
+  // middle tiles t0+1 .. t1-2 in ring order (buffers 1, 2, .., 0, 1, ..), in
+  // groups of NBUF with compile-time buffers; the few left over and the last
+  // tile take their buffer as a run-time value (there the compiler waits for
+  // in-flight tile loads before each LDS read: a few tiles per workgroup)
+  int t = t0 + 1;
+  for (; t + NBUF < t1; t += NBUF) {
+    tile(t, I1{}, FF{});
+    tile(t + 1, I2{}, FF{});
+    tile(t + 2, I0{}, FF{});
+  }
+  for (; t + 1 < t1; ++t) tile(t, (t - t0) % NBUF, FF{});
+  tile(t, (t - t0) % NBUF, TF{});
+  wait_vmcnt<0>();   // (loads past the range must land before the workgroup ends)
+  // drain: O1 += V^T P(last half, g1)
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if (i == 0) g2::mma_o_first(o[1][i & 3], vf[i], pc[1][i >> 2]);
+    else g2::mma_o(o[1][i & 3], vf[i], pc[1][i >> 2]);
+  }
+  g2::mfma_drain();
+
+#pragma unroll
+  for (int gr = 0; gr < 2; ++gr) {
+    const int ql = wave * 64 + gr * 32 + col;
+    const int q = qb * BMQ + ql;
+    const float l = l_run[gr] + __shfl_xor(l_run[gr], 32);
+    if (split >= 0) {
+      const int nsplit = (int)(gridDim.x - p.nreg) / 2;
+      float* po = p.part + part_o_off<DH>(split >> 1, split & 1, ql, BMQ);
+#pragma unroll
+      for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+        for (int rr = 0; rr < 4; ++rr) {
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = o[gr][dt][4 * rr + e];
+          *reinterpret_cast<f32x4*>(po + dt * 32 + 8 * rr + 4 * g) = v;
+        }
+      if (g == 0) {
+        float* pml = p.part + part_ml_off<DH>(nsplit, split >> 1, split & 1, ql, BMQ);
+        pml[0] = m_run[gr];
+        pml[1] = l;
+      }
+      continue;
+    }
+    if (q >= p.Lq) continue;
+    const float inv = 1.f / l;
+    T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
+#pragma unroll
+    for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+      for (int rr = 0; rr < 4; ++rr) {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[gr][dt][4 * rr + e] * inv);
+        *reinterpret_cast<bf16x4*>(dst + dt * 32 + 8 * rr + 4 * g) = v;
+      }
+  }
+}
+
+template <bool SC>
+void launch_g2(AttnParams<bf16> p, hipStream_t stream, int ncu) {
+  constexpr int BMQ = 256;
+  const int items = ((p.Lq + BMQ - 1) / BMQ) * p.H * p.B;
+  const int rem = ncu > 0 ? items % ncu : 0;
+  const int nfull = p.Lk / AT_BN;
+  int nsplit = 0;
+  if (p.part && rem > 0 && 2 * rem <= ncu && rem <= kMaxSplitItems && nfull >= 4) nsplit = rem;
+  p.nreg = items - nsplit;
+  p.split_tile = (nfull / 2) & ~1;
+  hipLaunchKernelGGL((flash_attn_g2_kernel<SC>), dim3(p.nreg + 2 * nsplit), dim3(256), 0, stream, p);
+  if (nsplit > 0)
+    hipLaunchKernelGGL((attn_merge_kernel<bf16, 128, BMQ>), dim3(nsplit), dim3(256), 0, stream, p, nsplit);
+}
+
 template <typename T, int DH, int W>
 void launch_w(AttnParams<T> p, bool q_scaled, hipStream_t stream, int ncu) {
   constexpr int BMQ = W * 32;
@@ -478,7 +1079,12 @@ void launch_dh(const AttnParams<T>& p, bool q_scaled, hipStream_t stream, int nc
   // (float32 keeps four waves: its head-128 kernel needs one wave per SIMD)
   if constexpr (sizeof(T) == 2) {
     if (p.Lk >= kLongKeys) {
-      launch_w<T, DH, 8>(p, q_scaled, stream, ncu);
+      if constexpr (DH == 128) {
+        if (q_scaled) launch_g2<true>(p, stream, ncu);
+        else launch_g2<false>(p, stream, ncu);
+      } else {
+        launch_w<T, DH, 8>(p, q_scaled, stream, ncu);
+      }
       return;
     }
   }
