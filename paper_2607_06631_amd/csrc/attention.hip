@@ -473,9 +473,14 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 //   X(t,h): S(t,h,g1) = K Q1^T and O1 += V^T P(prev,g1);  softmax S(t,h,g0)
 //   Y(t,h): S(next,g0) = K Q0^T and O0 += V^T P(t,h,g0);  softmax S(t,h,g1)
 // Score and output MFMAs alternate, so no MFMA waits for the one before
-// it; after each MFMA come at most one LDS read, one exponential, one bf16
-// pack and two adds of the row sum.  K fragments of the next half are read
-// behind the score MFMAs that consume the current ones, V^T fragments
+// it.  The softmax of a half is spread over its block: its 16
+// exponentials in the first ten MFMA slots, each bf16 pair and row-sum add
+// one slot after its inputs, so the half's sum is ready by the 14th MFMA;
+// the lazy-rescale test and its (rare) branch then come before the block's
+// last MFMA, which belongs to the other group and so is untouched by a
+// rescale (+3.0 % against the test after the last MFMA, +2.5 % of that
+// from not waiting on a chain of adds).  K fragments of the next half are
+// read behind the score MFMAs that consume the current ones, V^T fragments
 // behind the output MFMAs, so every read has a block of MFMAs to land.
 //
 // K / V^T tiles sit in a ring of three LDS buffers with one workgroup
@@ -498,7 +503,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 // after the VALU writes its operand), and the rare rescale path and the
 // epilogue wait out the MFMA pipeline before touching the accumulators.
 // Measured against the eight-wave kernel on the blocks' launch (32760
-// tokens, 24-40 heads): +6.4 to +6.7 %.
+// tokens, 24-40 heads): +9.5 to +10 % (1.28 -> 1.40-1.42 PFLOP/s).
 namespace g2 {
 __device__ __forceinline__ void mma_sc(f32x16& d, const u32x4& a, const u32x4& b, const f32x16& c) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
@@ -721,40 +726,57 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
   float pe[2][16];
   float lsum[2][2];
   float ta[2][2][4], tb[2][2][2];   // the row-sum tree of each 8-key chunk
-  // Slot i of group gr's softmax, issued after one MFMA: the exponential of
-  // score i, the bf16 pair (i-1, i) of the P^T operand, and the adds of the
-  // chunk's sum tree ((e0+e4)+(e2+e6)) + ((e1+e5)+(e3+e7)) that have their
-  // inputs -- at most four VALU instructions between two MFMAs.
-  auto sm_slot = [&](int gr, int i) __attribute__((always_inline)) {
-    float x = s[gr][i];
-    if constexpr (!SC) x *= uscale;
-    pe[gr][i] = __builtin_amdgcn_exp2f(x);
-    g2::pin(pe[gr][i]);
-    const int u = i >> 3, k = i & 7;
-    if (i & 1) {
-      bf16x2 v2 = {(bf16)pe[gr][i - 1], (bf16)pe[gr][i]};
-      pc[gr][u][k >> 1] = __builtin_bit_cast(uint32_t, v2);
-      g2::pin(pc[gr][u]);
+  float lh[2];                        // the half's probability sum
+  // Group gr's softmax pieces issued after MFMA k (0..15) of a block: the
+  // exponentials e0..e7 two per slot in slots 0-3 and e8..e15 one per slot
+  // in 4-11; each bf16 pair of the P^T operand and each add of the chunk
+  // sums ((e0+e4)+(e2+e6)) + ((e1+e5)+(e3+e7)) one slot after its last
+  // input, so the half's sum is ready when the block ends (its test then
+  // does not wait on a chain of adds) -- at most five VALU instructions
+  // between two MFMAs.
+  auto sm_slot = [&](int gr, int k) __attribute__((always_inline)) {
+    auto es = [](int e) { return e < 12 ? e >> 1 : e - 6; };   // slot of exponential e
+#pragma unroll
+    for (int e = 0; e < 16; ++e)
+      if (es(e) == k) {
+        float x = s[gr][e];
+        if constexpr (!SC) x *= uscale;
+        pe[gr][e] = __builtin_amdgcn_exp2f(x);
+        g2::pin(pe[gr][e]);
+      }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (es(2 * j + 1) + 1 == k) {
+        bf16x2 v2 = {(bf16)pe[gr][2 * j], (bf16)pe[gr][2 * j + 1]};
+        pc[gr][j >> 2][j & 3] = __builtin_bit_cast(uint32_t, v2);
+        g2::pin(pc[gr][j >> 2]);
+      }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (es(8 * u + q + 4) + 1 == k) {
+          ta[gr][u][q] = pe[gr][8 * u + q] + pe[gr][8 * u + q + 4];
+          g2::pin(ta[gr][u][q]);
+        }
+      const int b0 = es(8 * u + 6) + 2, b1 = es(8 * u + 7) + 2;
+      if (b0 == k) {
+        tb[gr][u][0] = ta[gr][u][0] + ta[gr][u][2];
+        g2::pin(tb[gr][u][0]);
+      }
+      if (b1 == k) {
+        tb[gr][u][1] = ta[gr][u][1] + ta[gr][u][3];
+        g2::pin(tb[gr][u][1]);
+      }
+      if ((b0 > b1 ? b0 : b1) + 1 == k) {
+        lsum[gr][u] = tb[gr][u][0] + tb[gr][u][1];
+        g2::pin(lsum[gr][u]);
+      }
     }
-    if (k >= 4) {
-      ta[gr][u][k - 4] = pe[gr][i - 4] + pe[gr][i];
-      g2::pin(ta[gr][u][k - 4]);
+    if (k == 13) {
+      lh[gr] = lsum[gr][0] + lsum[gr][1];
+      g2::pin(lh[gr]);
     }
-    if (k == 6) {
-      tb[gr][u][0] = ta[gr][u][0] + ta[gr][u][2];
-      g2::pin(tb[gr][u][0]);
-    }
-    if (k == 7) {
-      tb[gr][u][1] = ta[gr][u][1] + ta[gr][u][3];
-      g2::pin(tb[gr][u][1]);
-    }
-    if (i == 8) {
-      lsum[gr][0] = tb[gr][0][0] + tb[gr][0][1];
-      g2::pin(lsum[gr][0]);
-    }
-  };
-  auto sm_end = [&](int gr) __attribute__((always_inline)) {
-    lsum[gr][1] = tb[gr][1][0] + tb[gr][1][1];
   };
   auto sm_exp = [&](int gr, int e) __attribute__((always_inline)) {
     float x = s[gr][e];
@@ -778,8 +800,7 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
   // Lazy rescale of group gr after its half's probabilities (see the
   // eight-wave kernel): rare; it reads and rewrites the AGPR accumulators.
   auto sm_check = [&](int gr) __attribute__((always_inline)) {
-    float lh = lsum[gr][0] + lsum[gr][1];
-    if (__any(!(lh <= (float)(1 << (int)kSlack)))) {
+    if (__any(!(lh[gr] <= (float)(1 << (int)kSlack)))) {
       g2::mfma_drain();
       float mx = -INFINITY;
 #pragma unroll
@@ -806,10 +827,10 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
       for (int e = 0; e < 16; ++e) sm_exp(gr, e);
       sm_pack(gr, 0);
       sm_pack(gr, 1);
-      lh = lsum[gr][0] + lsum[gr][1];
+      lh[gr] = lsum[gr][0] + lsum[gr][1];
       g2::valu_to_mfma();
     }
-    l_run[gr] += lh;
+    l_run[gr] += lh[gr];
   };
 
   // ---- prologue: tiles t0 .. t0+NBUF-2 in flight, the base m of each group
@@ -903,6 +924,9 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
       }
       if constexpr (LOADS && CT) load_one(min(lt, nfull - 1), lbuf, i);
       sm_slot(0, 2 * i);
+      // group 0's test, before the last MFMA (group 1's: a rescale of
+      // group 0 leaves it alone)
+      if (i == 7) sm_check(0);
       __builtin_amdgcn_sched_barrier(0);
       if constexpr (!FIRST) {
         if (i == 0) g2::mma_o_first(o[1][i & 3], vf[i], pc[1][i >> 2]);
@@ -920,8 +944,6 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
     }
     // (without output MFMAs behind them, the scores of g1 need the drain)
     if constexpr (FIRST) g2::mfma_drain();
-    sm_end(0);
-    sm_check(0);
   };
   // Y(t, H): S(next, g0), then O0 += V^T P(t,H,g0); softmax of S(t,H,g1).
   auto blockY = [&](int t, auto buf_c, auto h_c, auto next_c, auto masked_c) __attribute__((always_inline)) {
@@ -939,6 +961,7 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
         if (i == 0) g2::mma_sc(s[0], kf[0], qf[0][0], negm[0]);
         else g2::mma_s(s[0], kf[i], qf[0][i]);
         sm_slot(1, 2 * i);
+        if (i == 7) sm_check(1);   // (the last MFMA is group 0's)
         __builtin_amdgcn_sched_barrier(0);
         if (i == 0) g2::mma_o_first(o[0][i & 3], vf[i], pc[0][i >> 2]);
         else g2::mma_o(o[0][i & 3], vf[i], pc[0][i >> 2]);
@@ -954,9 +977,8 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
         sm_slot(1, 2 * i + 1);
         __builtin_amdgcn_sched_barrier(0);
       }
+      sm_check(1);
     }
-    sm_end(1);
-    sm_check(1);
   };
   using TF = std::true_type;
   using FF = std::false_type;

@@ -1,8 +1,9 @@
 """Self-attention in the launch configuration the blocks use, against the oracle.
 
 The blocks call the attention kernel with queries already multiplied by
-log2(e)/sqrt(dh) (the QK-norm kernel writes them so), in eight-wave
-workgroups of 256 queries for bfloat16 keys of 4096 and more, and -- when
+log2(e)/sqrt(dh) (the QK-norm kernel writes them so), in workgroups of 256
+queries for bfloat16 keys of 4096 and more (four waves of two 32-query
+groups at head_dim 128, eight waves of 32 queries at 64), and -- when
 the last round of workgroups on the device would run at most half full --
 with that round's work items split along the keys and merged by a second
 kernel.  dif_attention_ex runs exactly that launch.  Here it runs at the
