@@ -476,10 +476,11 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 // it.  The softmax of a half is spread over its block: its 16
 // exponentials in the first ten MFMA slots, each bf16 pair and row-sum add
 // one slot after its inputs, so the half's sum is ready by the 14th MFMA;
-// the lazy-rescale test and its (rare) branch then come before the block's
-// last MFMA, which belongs to the other group and so is untouched by a
-// rescale (+3.0 % against the test after the last MFMA, +2.5 % of that
-// from not waiting on a chain of adds).  K fragments of the next half are
+// the lazy-rescale test and its (rare, out-of-line) branch then come
+// before the block's last MFMA, which belongs to the other group and so is
+// untouched by a rescale (+3.0 % against the test after the last MFMA,
+// +2.5 % of that from not waiting on a chain of adds; +1.5 % more with the
+// rescale block laid out off the straight path).  K fragments of the next half are
 // read behind the score MFMAs that consume the current ones, V^T fragments
 // behind the output MFMAs, so every read has a block of MFMAs to land.
 //
@@ -502,8 +503,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 // explicit wait precedes the first output MFMA of a block (two wait states
 // after the VALU writes its operand), and the rare rescale path and the
 // epilogue wait out the MFMA pipeline before touching the accumulators.
+// The tile loads' buffer descriptors span exactly one full tile (a
+// multiply-add of scalars per tile instead of a 64-bit bound clamp, +1.3 %).
 // Measured against the eight-wave kernel on the blocks' launch (32760
-// tokens, 24-40 heads): +9.5 to +10 % (1.28 -> 1.40-1.42 PFLOP/s).
+// tokens, 24-40 heads): +11 to +12 % (1.28 -> 1.42-1.44 PFLOP/s).
 namespace g2 {
 __device__ __forceinline__ void mma_sc(f32x16& d, const u32x4& a, const u32x4& b, const f32x16& c) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
@@ -639,16 +642,22 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
   // one direct-to-LDS instruction j of tile kt (j < KI: K rows, else V^T
   // rows), LDS address from the wave index in an SGPR
   [[maybe_unused]] const int wave_s = __builtin_amdgcn_readfirstlane(wave) & (W - 1);   // (known range 0..W-1)
+  // (full tiles only -- the key-tail tile goes through registers -- so the
+  // descriptors span exactly the tile: every access is inside it)
+  const uint32_t k_tile_bytes = (uint32_t)(AT_BN * p.ldk * ES);
+  const uint32_t v_tile_bytes = (uint32_t)(DH * p.ldvt * ES);
   auto load_one = [&](int kt, int buf, int j) __attribute__((always_inline)) {
 #if defined(__HIP_DEVICE_COMPILE__)
     typedef __attribute__((address_space(3))) void lds_t;
-    const int key0 = kt * AT_BN;
     if (j < KI) {
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(k_rsrc(key0), (lds_t*)&kbuf(buf)[(j * W + wave_s) * KRPI][0], 16,
+      const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<T*>(kbase) + (uint64_t)(uint32_t)kt * (AT_BN * (uint64_t)p.ldk), (short)0, k_tile_bytes,
+          kRsrcWord3);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_t*)&kbuf(buf)[(j * W + wave_s) * KRPI][0], 16,
                                                kd_off[j], 0, 0, 0);
     } else {
       const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<T*>(vbase + key0), (short)0, (uint32_t)(v_bytes - (int64_t)key0 * ES), kRsrcWord3);
+          const_cast<T*>(vbase) + (uint32_t)kt * AT_BN, (short)0, v_tile_bytes, kRsrcWord3);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_t*)&vbuf(buf)[((j - KI) * W + wave_s) * VRPI][0], 16,
                                                vd_off[j - KI], 0, 0, 0);
     }
@@ -800,7 +809,7 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
   // Lazy rescale of group gr after its half's probabilities (see the
   // eight-wave kernel): rare; it reads and rewrites the AGPR accumulators.
   auto sm_check = [&](int gr) __attribute__((always_inline)) {
-    if (__any(!(lh[gr] <= (float)(1 << (int)kSlack)))) {
+    if (__builtin_expect(__any(!(lh[gr] <= (float)(1 << (int)kSlack))), 0)) {
       g2::mfma_drain();
       float mx = -INFINITY;
 #pragma unroll
