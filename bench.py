@@ -42,9 +42,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "ee9eaaa578585787afb49ad99150ea906a78bfc3758fc7f0a53c9bc36a35d09b",
-    "fetch_bytes": 1107788.9640625 * 1024 / 0.500,
-    "write_bytes": 355332.070703125 * 1024 / 1.000,
+    "sha256": "0f68bef373897a4d977bb3aa6175d8682ba598c8bc46c3496e1d560722e6a25b",
+    "fetch_bytes": 1103438.836328125 * 1024 / 0.500,
+    "write_bytes": 258161.60703125 * 1024 / 1.000,
 }
 
 
