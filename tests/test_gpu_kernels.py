@@ -159,9 +159,21 @@ def test_attention_matches_oracle(dtype, dh, Lq, Lk):
 
 @pytest.mark.parametrize("dh", [128, 64])
 def test_attention_long_keys_online_softmax(dh):
-    say(f"attention bf16 long keys dh={dh} (eight-wave workgroups)")
+    say(f"attention bf16 long keys dh={dh} (long-key kernels)")
     # sharp scores that keep moving the running max across many key tiles;
-    # Lk >= 4096 takes the eight-wave kernel, Lq = 300 ends in a partial
-    # 256-query block and Lk = 4099 in a 3-key tile
+    # Lk >= 4096 takes the long-key kernels (two query groups per wave at
+    # head_dim 128, eight waves at 64), Lq = 300 ends in a partial 256-query
+    # block and Lk = 4099 in a 3-key tile
     err = _attn_case("bf16", dh, 2, 300, 4099, Bn=1, qscale=4.0, seed=11)
+    assert err <= 2e-2
+
+
+@pytest.mark.parametrize("Lk", [4160, 4165, 4257])
+def test_attention_long_keys_ring_leftovers(Lk):
+    """The two-group kernel runs its middle key tiles in groups of three
+    (one per LDS ring slot) and the rest, with the last tile, through a
+    run-time slot: 4160 keys (65 full tiles) leave none, 4165 (a 5-key
+    tail) one, 4257 (a 33-key tail) two."""
+    say(f"attention bf16 dh=128 Lk={Lk} (ring leftovers)")
+    err = _attn_case("bf16", 128, 2, 300, Lk, Bn=2, qscale=4.0, seed=Lk)
     assert err <= 2e-2
