@@ -87,6 +87,61 @@ __device__ __forceinline__ int key_slot(int kappa) {
   return 8 * k + 4 * gq + j;
 }
 
+// Writes the 32 output rows a wave holds (query lane % 32; accumulator
+// o[dt], register 4 rr + e, holds dim 32 dt + 8 rr + 4 g + e with
+// g = lane / 32), times inv and converted to T, to dst (row stride ld;
+// rows >= nrows are skipped) through the wave's own LDS region of
+// 32 * DH * sizeof(T) bytes, which must be free.  Direct stores would put
+// 32 rows into every store instruction; staged, each instruction writes
+// whole rows.  The staging swizzles a row's 16-byte chunks by the row
+// (and, for 2-byte T, the two 8-byte halves of a chunk by the next row
+// bit), so the 8-byte column writes and the row reads are free of bank
+// conflicts at head_dim 128.  A wave's LDS instructions execute in order:
+// between its writes and reads a wavefront-scope fence (no barrier) keeps
+// the compiler from reordering them.
+template <typename T, int DH>
+__device__ __forceinline__ void store_rows_staged(const f32x16 (&o)[DH / 32], float inv, char* stage,
+                                                  T* dst, int64_t ld, int nrows, int lane) {
+  constexpr int ES = (int)sizeof(T);
+  constexpr int RB = DH * ES;     // bytes per row
+  constexpr int CPR = RB / 16;    // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;   // rows per read-back instruction
+  static_assert(RPI * CPR == 64 && 32 % RPI == 0, "row staging split");
+  // (opaque, so no address arithmetic of this epilogue is merged with, and
+  // kept live from, the key loop's)
+  asm volatile("" : "+v"(lane));
+  const int col = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int dt = 0; dt < DH / 32; ++dt)
+#pragma unroll
+    for (int rr = 0; rr < 4; ++rr) {
+      const int byte = (dt * 32 + 8 * rr + 4 * g) * ES;
+      if constexpr (ES == 4) {
+        f32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rr + e] * inv;
+        *reinterpret_cast<f32x4*>(stage + col * RB + 16 * ((byte / 16) ^ (col % CPR))) = v;
+      } else {
+        bf16x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[dt][4 * rr + e] * inv);
+        const int half = ((byte / 8) & 1) ^ ((col / CPR) & 1);
+        *reinterpret_cast<bf16x4*>(stage + col * RB + 16 * ((byte / 16) ^ (col % CPR)) + 8 * half) = v;
+      }
+    }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+#pragma unroll
+  for (int i = 0; i < 32 / RPI; ++i) {
+    const int row = i * RPI + lane / CPR, c = lane % CPR;
+    u32x4 v = *reinterpret_cast<const u32x4*>(stage + row * RB + 16 * (c ^ (row % CPR)));
+    if constexpr (ES == 2) {
+      if (((i * RPI) / CPR) & 1) v = u32x4{v[2], v[3], v[0], v[1]};   // (uniform per instruction)
+    }
+    if (row < nrows) *reinterpret_cast<u32x4*>(reinterpret_cast<char*>(dst + row * ld) + 16 * c) = v;
+  }
+}
+
 // SC: queries arrive pre-multiplied by log2(e)/sqrt(dh); AT_WAVES waves per
 // workgroup (4 or 8: two waves per SIMD either way).
 template <typename T, int DH, bool SC, int AT_WAVES>
@@ -384,7 +439,6 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
     else tile(kt, B0{}, std::true_type{});
   }
 
-  const int q = qb * BMQ + wave * 32 + col;
   const float l = l_run + __shfl_xor(l_run, 32);
   if (split >= 0) {
     // unnormalised sums and this half's (m, l), combined by attn_merge_kernel
@@ -407,26 +461,15 @@ __global__ __launch_bounds__(64 * AT_WAVES, 8 / AT_WAVES) void flash_attn_kernel
     }
     return;
   }
-  if (q >= p.Lq) return;
+  // Output rows through LDS (free since the last tile's barrier).  A lane
+  // holds four consecutive dims of its query per register group, so direct
+  // stores would put 32 rows in every store instruction; staged, each
+  // instruction writes whole rows (full 128-byte lines).
   const float inv = 1.f / l;
-  T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
-#pragma unroll
-  for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-    for (int rr = 0; rr < 4; ++rr) {
-      const int d = dt * 32 + 8 * rr + 4 * g;
-      if constexpr (sizeof(T) == 4) {
-        f32x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = o[dt][4 * rr + e] * inv;
-        *reinterpret_cast<f32x4*>(dst + d) = v;
-      } else {
-        bf16x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[dt][4 * rr + e] * inv);
-        *reinterpret_cast<bf16x4*>(dst + d) = v;
-      }
-    }
+  store_rows_staged<T, DH>(o, inv, wave < 4 ? reinterpret_cast<char*>(&ks_[0][0][0]) + wave * 32 * DH * (int)sizeof(T)
+                                             : reinterpret_cast<char*>(&vs_[0][0][0]) + (wave - 4) * 32 * DH * (int)sizeof(T),
+                           p.O + ((int64_t)b * p.Lq + qb * BMQ + wave * 32) * p.ldo + h * DH, p.ldo,
+                           min(32, p.Lq - (qb * BMQ + wave * 32)), lane);
 }
 
 // Combines the two key halves of each split item: with m = max(m0, m1) and
@@ -510,6 +553,10 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 namespace g2 {
 __device__ __forceinline__ void mma_sc(f32x16& d, const u32x4& a, const u32x4& b, const f32x16& c) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %3" : "=&v"(d) : "v"(a), "a"(b), "v"(c));
+}
+// the first k-step with a zero accumulator (an inline constant: no registers)
+__device__ __forceinline__ void mma_s0(f32x16& d, const u32x4& a, const u32x4& b) {
+  asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, 0" : "=&v"(d) : "v"(a), "a"(b));
 }
 __device__ __forceinline__ void mma_s(f32x16& d, const u32x4& a, const u32x4& b) {
   asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+v"(d) : "v"(a), "a"(b));
@@ -837,6 +884,9 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
       sm_pack(gr, 0);
       sm_pack(gr, 1);
       lh[gr] = lsum[gr][0] + lsum[gr][1];
+      g2::pin(negm[gr]);
+      g2::pin(pc[gr][0]);
+      g2::pin(pc[gr][1]);
       g2::valu_to_mfma();
     }
     l_run[gr] += lh[gr];
@@ -851,14 +901,11 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
   wait_vmcnt<0>();
   __syncthreads();
   {
-    f32x16 z;
-#pragma unroll
-    for (int r = 0; r < 16; ++r) z[r] = 0.f;
 #pragma unroll
     for (int i = 0; i < NQS; ++i) read_k(I0{}, 0, i);
 #pragma unroll
     for (int gr = 0; gr < 2; ++gr) {
-      g2::mma_sc(s[gr], kf[0], qf[gr][0], z);
+      g2::mma_s0(s[gr], kf[0], qf[gr][0]);
 #pragma unroll
       for (int i = 1; i < NQS; ++i) g2::mma_s(s[gr], kf[i], qf[gr][i]);
     }
@@ -873,6 +920,9 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
 #pragma unroll
       for (int r = 0; r < 16; ++r) negm[gr][r] = -m_run[gr] / uscale;
     }
+    // (the pins keep the VALU writes of negm ahead of the wait states)
+    g2::pin(negm[0]);
+    g2::pin(negm[1]);
     g2::valu_to_mfma();
     // S(t0, 0, g0) against the base
     g2::mma_sc(s[0], kf[0], qf[0][0], negm[0]);
@@ -1025,14 +1075,17 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
     else g2::mma_o(o[1][i & 3], vf[i], pc[1][i >> 2]);
   }
   g2::mfma_drain();
+  // negm is the accumulator input of the last score MFMAs: live until the
+  // drain, so its registers are not rewritten while they may be read
+  g2::pin(negm[0]);
+  g2::pin(negm[1]);
 
+  if (split >= 0) {
+    const int nsplit = (int)(gridDim.x - p.nreg) / 2;
 #pragma unroll
-  for (int gr = 0; gr < 2; ++gr) {
-    const int ql = wave * 64 + gr * 32 + col;
-    const int q = qb * BMQ + ql;
-    const float l = l_run[gr] + __shfl_xor(l_run[gr], 32);
-    if (split >= 0) {
-      const int nsplit = (int)(gridDim.x - p.nreg) / 2;
+    for (int gr = 0; gr < 2; ++gr) {
+      const int ql = wave * 64 + gr * 32 + col;
+      const float l = l_run[gr] + __shfl_xor(l_run[gr], 32);
       float* po = p.part + part_o_off<DH>(split >> 1, split & 1, ql, BMQ);
 #pragma unroll
       for (int dt = 0; dt < DH / 32; ++dt)
@@ -1048,20 +1101,23 @@ __global__ __launch_bounds__(256, 1) void flash_attn_g2_kernel(AttnParams<bf16> 
         pml[0] = m_run[gr];
         pml[1] = l;
       }
-      continue;
     }
-    if (q >= p.Lq) continue;
-    const float inv = 1.f / l;
-    T* dst = p.O + ((int64_t)b * p.Lq + q) * p.ldo + h * DH;
+    return;
+  }
+  // Output rows through LDS: once every wave is past its last fragment
+  // reads, each wave stages its 64 rows in a 16 KB ring slot of its own.
+  __syncthreads();
+  char* stage = reinterpret_cast<char*>(wave == 0   ? &ks0_[0][0]
+                                        : wave == 1 ? &ks1_[0][0]
+                                        : wave == 2 ? &ks2_[0][0]
+                                                    : &vs0_[0][0]);
 #pragma unroll
-    for (int dt = 0; dt < DH / 32; ++dt)
-#pragma unroll
-      for (int rr = 0; rr < 4; ++rr) {
-        bf16x4 v;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = (bf16)(o[gr][dt][4 * rr + e] * inv);
-        *reinterpret_cast<bf16x4*>(dst + dt * 32 + 8 * rr + 4 * g) = v;
-      }
+  for (int gr = 0; gr < 2; ++gr) {
+    const int q0 = qb * BMQ + wave * 64 + gr * 32;
+    const float l = l_run[gr] + __shfl_xor(l_run[gr], 32);
+    store_rows_staged<T, DH>(o[gr], 1.f / l, stage + gr * 32 * DH * (int)sizeof(T),
+                             p.O + ((int64_t)b * p.Lq + q0) * p.ldo + h * DH, p.ldo,
+                             min(32, p.Lq - q0), lane);
   }
 }
 
