@@ -42,9 +42,9 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "0f68bef373897a4d977bb3aa6175d8682ba598c8bc46c3496e1d560722e6a25b",
-    "fetch_bytes": 1103438.836328125 * 1024 / 0.500,
-    "write_bytes": 258161.60703125 * 1024 / 1.000,
+    "sha256": "379b0f6a2fff75cc82d602a782fc0203fad2d4c6d428a6e425da698fd61dcb89",
+    "fetch_bytes": 1103487.105078125 * 1024 / 0.500,
+    "write_bytes": 255131.5083984375 * 1024 / 1.000,
 }
 
 
