@@ -69,6 +69,14 @@ def parse():
                     help="project every layer's text keys and values once per video "
                          "(timed apart, reported as text_cache_build_ms) and run the cached "
                          "step; the step's FLOP count then leaves out that projection")
+    ap.add_argument("--gemm-vs-library", action="store_true",
+                    help="instead of the step: time this library's GEMM (plain store "
+                         "epilogue) against torch's bf16 linear (the platform BLAS) on the "
+                         "step's projection shapes, and print one JSON line")
+    ap.add_argument("--mfma-ceiling", action="store_true",
+                    help="instead of the step: time the library's pure-MFMA probe (every CU "
+                         "issuing the bf16 MFMA the kernels use, no memory traffic) and print "
+                         "the sustained TFLOP/s as one JSON line")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="before the steps, run one plain device copy of this many MiB "
                          "(the reference dispatch that scales HBM byte counters)")
@@ -331,6 +339,100 @@ def run_blocks(args, cfg):
     print(json.dumps(out))
 
 
+def gemm_vs_library(args, cfg):
+    """The step's projection GEMMs at full width (M = the video tokens; the
+    first step structure keeps every head and FFN channel): this library's
+    GEMM with the plain store epilogue against torch.nn.functional.linear
+    in bf16, which calls the platform BLAS.  Same operands, alternating
+    launches, HIP events; the outputs are compared (both accumulate in
+    float32 and round to bf16)."""
+    import torch
+    import torch.nn.functional as F
+
+    from paper_2607_06631_amd import binding as B
+
+    M, D, Fd = cfg.seq_len, cfg.dim, cfg.ffn_dim
+    shapes = [("qkv", 3 * D, D), ("out_proj", D, D), ("ffn1", Fd, D), ("ffn2", D, Fd)]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    reps = max(args.steps, 3)
+    out = {}
+    tot = {"dif": 0.0, "lib": 0.0, "flop": 0.0}
+    for name, N, K in shapes:
+        A = torch.randn((M, K), generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+        W = (torch.randn((N, K), generator=gen, device="cuda", dtype=torch.float32) * 0.02).to(torch.bfloat16)
+        C_dif = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        runs = {"dif": lambda: B.dif_gemm(A, W, C_dif), "lib": lambda: F.linear(A, W)}
+        for _ in range(max(args.warmup, 1)):
+            for f in runs.values():
+                f()
+        times = {k: [] for k in runs}
+        for _ in range(reps):
+            for k, f in runs.items():
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                f()
+                e1.record()
+                torch.cuda.synchronize()
+                times[k].append(e0.elapsed_time(e1))
+        C_lib = F.linear(A, W)
+        torch.cuda.synchronize()
+        diff = ((C_dif.float() - C_lib.float()).abs().max() / C_lib.float().abs().max()).item()
+        flop = 2.0 * M * N * K
+        row = {"M": M, "N": N, "K": K, "max_rel_diff": diff}
+        for k in runs:
+            ms = sorted(times[k])[len(times[k]) // 2]
+            row[f"{k}_ms"] = round(ms, 4)
+            row[f"{k}_tflops"] = round(flop / ms / 1e9, 1)
+            tot[k] += ms
+        row["dif_over_lib"] = round(row["lib_ms"] / row["dif_ms"], 3)
+        tot["flop"] += flop
+        out[name] = row
+        log(f"bench: {name} {row}")
+        del A, W, C_dif, C_lib
+    print(json.dumps({
+        "metric": "projection GEMM TFLOP/s, this library against the platform BLAS",
+        "library": f"torch.nn.functional.linear (bf16, blas backend "
+                   f"{torch.backends.cuda.preferred_blas_library()})",
+        "shapes": out,
+        "dif_tflops": round(tot["flop"] / tot["dif"] / 1e9, 1),
+        "lib_tflops": round(tot["flop"] / tot["lib"] / 1e9, 1),
+        "dif_over_lib": round(tot["lib"] / tot["dif"], 3),
+        "reps": reps, "data": "synthetic"}))
+
+
+def mfma_ceiling(args):
+    """The sustained rate of the bf16 MFMA all the kernels use, with every CU
+    busy and nothing else running (the chip's power limit sets the clock):
+    the ceiling against which the kernels' fraction of the 2.5 PFLOP/s
+    nominal peak is read."""
+    import torch
+
+    from paper_2607_06631_amd import binding as B
+
+    sink = torch.zeros(1, device="cuda", dtype=torch.float32)
+    iters = 300000   # about 0.1 s per launch
+    for _ in range(max(args.warmup, 1)):
+        B.dif_mfma_probe(iters, sink)
+    torch.cuda.synchronize()
+    rates = []
+    for _ in range(max(args.steps, 3)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fl = B.dif_mfma_probe(iters, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        rates.append(fl / e0.elapsed_time(e1) / 1e9)
+    rates.sort()
+    med = rates[len(rates) // 2]
+    print(json.dumps({"metric": "sustained bf16 MFMA rate (v_mfma_f32_32x32x16_bf16, all CUs, "
+                                "no memory traffic)",
+                      "tflops_median": round(med, 1), "tflops_min": round(rates[0], 1),
+                      "tflops_max": round(rates[-1], 1),
+                      "frac_nominal_peak": round(med / PEAK_BF16_TFLOPS, 4),
+                      "launches": len(rates), "flop_per_launch": fl}))
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -350,6 +452,12 @@ def main():
 
     cfg = get_config(args.workload)
     torch.cuda.set_device(0)
+    if args.gemm_vs_library:
+        gemm_vs_library(args, cfg)
+        return
+    if args.mfma_ceiling:
+        mfma_ceiling(args)
+        return
     if cfg.name in ("wan14b_block", "wan1.3b_block"):
         run_blocks(args, cfg)
         return

@@ -443,6 +443,19 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
                                    int64_t ldvt, void* O, int64_t ldo, int32_t B, int32_t Lq,
                                    int32_t Lk, int32_t n_heads, dif_stream stream);
 
+/* The matrix cores' sustained rate, for the roofline's context: launches
+ * (on `stream`, asynchronously) a kernel that keeps every CU's matrix units
+ * issuing v_mfma_f32_32x32x16_bf16 -- the instruction every MFMA kernel of
+ * this library uses -- on random operands for about `iters` x 32 MFMAs per
+ * wave, two workgroups of four waves per CU, with no memory traffic, and
+ * sets *flops to the FLOPs it performs (iters rounded up to a multiple of 4).
+ * Time it with events on the same stream: FLOPs / time is the rate the chip
+ * holds under its power limit with nothing but MFMAs to do.  `sink` is a
+ * device float the kernel may write (it never does for any realistic
+ * result; it keeps the work from being optimised away).  Errors: DIF_E_ARG
+ * for iters < 1 or a null pointer, DIF_E_UNSUPPORTED off gfx950. */
+dif_status dif_mfma_probe(int32_t iters, float* sink, double* flops, dif_stream stream);
+
 /* ------------------------------------------------------------------------
  * Kernel timing: while enabled, every kernel the library launches is
  * bracketed by HIP events on its stream, grouped by kind, with the kind's

@@ -114,6 +114,7 @@ def lib():
                                        i32, i32, vp, sz, vp]),
             "dif_attention_ex_static": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32,
                                               i32, i32, i32, vp]),
+            "dif_mfma_probe": (i32, [i32, vp, C.POINTER(C.c_double), vp]),
             "dif_profile_enable": (i32, [i32]),
             "dif_profile_reset": (i32, []),
             "dif_profile_kind_name": (C.c_char_p, [i32]),
@@ -467,6 +468,14 @@ def dif_attention(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim:
 
 
 DIF_ATTN_Q_PRESCALED = 1
+
+
+def dif_mfma_probe(iters: int, sink, stream=None) -> float:
+    """Launches the sustained-MFMA-rate kernel; returns its FLOPs (time it
+    with events on the same stream).  `sink`: a float32 device tensor."""
+    fl = C.c_double()
+    _check(lib().dif_mfma_probe(iters, sink.data_ptr(), C.byref(fl), _stream(stream)))
+    return fl.value
 
 
 def dif_attention_split_bytes(head_dim: int) -> int:

@@ -1391,6 +1391,19 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
   GUARD_END
 }
 
+dif_status dif_mfma_probe(int32_t iters, float* sink, double* flops, dif_stream stream) {
+  GUARD_BEGIN
+  if (iters < 1) return fail(DIF_E_ARG, "iters must be >= 1");
+  if (!sink || !flops) return fail(DIF_E_ARG, "null argument");
+  if (!is_gfx950()) return fail(DIF_E_UNSUPPORTED, "current HIP device is not gfx950");
+  int dev = 0, ncu = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  HIP_TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
+  HIP_TRY(dif::launch_mfma_probe(iters, sink, ncu, static_cast<hipStream_t>(stream), flops));
+  return DIF_OK;
+  GUARD_END
+}
+
 dif_status dif_profile_enable(int32_t on) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   g_prof.on = on != 0;

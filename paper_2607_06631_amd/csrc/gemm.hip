@@ -602,6 +602,56 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
   return hipGetLastError();
 }
 
+// The chip's sustained MFMA rate with nothing else running: every CU holds
+// two workgroups of four waves, each wave issuing independent
+// v_mfma_f32_32x32x16_bf16 on eight accumulators (operands from a hash of
+// the thread: random-looking bf16 of magnitude ~1, rotated between
+// iterations), no memory traffic.  The result only decides whether a
+// never-taken store happens, so the work cannot be optimised away.  The
+// rate it reaches is the ceiling the power limit leaves for MFMA-bound
+// kernels (the clock drops below its 2.4 GHz maximum under this load).
+__global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters4, float* sink) {
+  const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+  bf16x8 a[4], b[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t h = (t * 8u + (uint32_t)(i * 8 + e)) * 2654435761u;
+      h ^= h >> 15;
+      h *= 2246822519u;
+      h ^= h >> 13;
+      a[i][e] = (bf16)(((float)(h & 0xffff) - 32768.f) / 32768.f);
+      b[i][e] = (bf16)(((float)(h >> 16) - 32768.f) / 32768.f);
+    }
+  f32x16 c[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) c[j][r] = 0.f;
+  for (int it = 0; it < iters4; ++it) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(j + u) & 3], b[j & 3], c[j], 0, 0, 0);
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sum += c[j][r];
+  if (sum == 1234567.f) *sink = sum;
+}
+
+hipError_t launch_mfma_probe(int iters, float* sink, int ncu, hipStream_t stream, double* flops) {
+  const int iters4 = (iters + 3) / 4;
+  const int blocks = 2 * ncu;
+  *flops = (double)blocks * 4 * (4.0 * iters4) * 8 * (2.0 * 32 * 32 * 16);
+  hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(256), 0, stream, iters4, sink);
+  return hipGetLastError();
+}
+
 #define INST(T, OutT)                                                                         \
   template hipError_t launch_gemm<T, OutT>(const T*, int64_t, const T*, int64_t, OutT*, int64_t, \
                                            int, int, int, int, const float*, const float*,    \

@@ -344,6 +344,15 @@ void operator_cases(Arena& ar) {
                   nullptr, nullptr) == DIF_E_ARG);
   EXPECT(dif_gemm(DIF_BF16, DIF_BF16, (char*)A + 2, 128, Bm, 128, Cm, 256, 256, 256, 128, 0, nullptr,
                   nullptr, nullptr, nullptr) == DIF_E_ARG);
+  // the MFMA-rate probe: FLOP count, argument errors
+  {
+    float* sink = static_cast<float*>(ar.get(sizeof(float)));
+    double fl = 0;
+    EXPECT(dif_mfma_probe(5, sink, &fl, nullptr) == DIF_OK && fl > 0);
+    EXPECT(dif_mfma_probe(0, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(5, nullptr, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(5, sink, nullptr, nullptr) == DIF_E_ARG);
+  }
   // attention: plain and the block's launch (pre-scaled queries, split workspace)
   const int Bn = 1, L = 300, H = 3, dh = 128;
   void* Q = ar.get((size_t)L * H * dh * 2);

@@ -177,3 +177,28 @@ def test_attention_long_keys_ring_leftovers(Lk):
     say(f"attention bf16 dh=128 Lk={Lk} (ring leftovers)")
     err = _attn_case("bf16", 128, 2, 300, Lk, Bn=2, qscale=4.0, seed=Lk)
     assert err <= 2e-2
+
+
+@pytest.mark.gpu
+def test_mfma_probe_rate_is_plausible():
+    """dif_mfma_probe: FLOPs as documented (iters rounded up to a multiple of
+    4; 2 workgroups x 4 waves per CU x 8 MFMAs of 32x32x16 per iteration),
+    a rate between a tenth and all of the 2.5 PFLOP/s nominal peak, and the
+    guard store never taken; a bad argument is rejected."""
+    import torch
+    say("mfma probe")
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    sink = torch.zeros(1, device="cuda", dtype=torch.float32)
+    fl = B.dif_mfma_probe(1001, sink)
+    assert fl == 2 * ncu * 4 * 1004 * 8 * 2 * 32 * 32 * 16
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    fl = B.dif_mfma_probe(2000, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    tflops = fl / e0.elapsed_time(e1) / 1e9
+    say(f"  {tflops:.1f} TFLOP/s")
+    assert 250.0 < tflops <= 2500.0
+    assert sink.item() == 0.0
+    with pytest.raises(B.DifError):
+        B.dif_mfma_probe(0, sink)
