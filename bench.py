@@ -42,7 +42,7 @@ ATTN_TRAFFIC = {
     "kernel": "attn_self",
     "workload": "wan14b_480p",
     "sources": ("paper_2607_06631_amd/csrc/attention.hip", "paper_2607_06631_amd/csrc/common.h"),
-    "sha256": "379b0f6a2fff75cc82d602a782fc0203fad2d4c6d428a6e425da698fd61dcb89",
+    "sha256": "6464fc09cbbe108547641a49baaf2282ed1af408c8b706b33e64c5f012c99558",
     "fetch_bytes": 1103487.105078125 * 1024 / 0.500,
     "write_bytes": 255131.5083984375 * 1024 / 1.000,
 }

@@ -546,6 +546,14 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnParams<T> p, int ns
 // explicit wait precedes the first output MFMA of a block (two wait states
 // after the VALU writes its operand), and the rare rescale path and the
 // epilogue wait out the MFMA pipeline before touching the accumulators.
+// Plain VALU code may still be scheduled across those waits, and a register
+// an MFMA reads may be reused right after it, so values the VALU writes for
+// an MFMA (-m, recomputed probabilities) are pinned by empty register
+// constraints ahead of each wait, -m stays live to the end of the kernel
+// (an MFMA reads its accumulator input during its passes), and the first
+// k-step of the prologue takes a zero accumulator as an inline constant.
+// tests/test_mfma_hazards.py scans the compiled kernel for all three
+// hazard patterns.
 // The tile loads' buffer descriptors span exactly one full tile (a
 // multiply-add of scalars per tile instead of a 64-bit bound clamp, +1.3 %).
 // Measured against the eight-wave kernel on the blocks' launch (32760
