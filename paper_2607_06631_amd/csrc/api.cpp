@@ -1393,7 +1393,7 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
 
 dif_status dif_mfma_probe(int32_t iters, float* sink, double* flops, dif_stream stream) {
   GUARD_BEGIN
-  if (iters < 1) return fail(DIF_E_ARG, "iters must be >= 1");
+  if (iters < 1 || iters > 10000000) return fail(DIF_E_ARG, "iters %d outside 1 .. 10^7", iters);
   if (!sink || !flops) return fail(DIF_E_ARG, "null argument");
   if (!is_gfx950()) return fail(DIF_E_UNSUPPORTED, "current HIP device is not gfx950");
   int dev = 0, ncu = 0;

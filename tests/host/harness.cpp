@@ -350,6 +350,7 @@ void operator_cases(Arena& ar) {
     double fl = 0;
     EXPECT(dif_mfma_probe(5, sink, &fl, nullptr) == DIF_OK && fl > 0);
     EXPECT(dif_mfma_probe(0, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(10000001, sink, &fl, nullptr) == DIF_E_ARG);
     EXPECT(dif_mfma_probe(5, nullptr, &fl, nullptr) == DIF_E_ARG);
     EXPECT(dif_mfma_probe(5, sink, nullptr, nullptr) == DIF_E_ARG);
   }
