@@ -35,22 +35,29 @@ namespace dif {
 // multiplies A row block i / TN by B column block i % TN): the value is a
 // row block index (< TM) or TM + a column block index.  For 4 x 2 blocks:
 // A0 B0 B1 A1 A2 A3.
+// (a table built at compile time: indexing it with an unrolled loop's
+// counter gives constants, so the fragment arrays stay in registers)
 template <int TM, int TN>
-__device__ constexpr int first_use(int k) {
+struct FirstUse {
+  int v[TM + TN];
+};
+template <int TM, int TN>
+__host__ __device__ constexpr FirstUse<TM, TN> first_use_table() {
+  FirstUse<TM, TN> t{};
   bool seen[TM + TN] = {};
   int n = 0;
   for (int i = 0; i < TM * TN; ++i) {
     const int a = i / TN, b = TM + i % TN;
     if (!seen[a]) {
       seen[a] = true;
-      if (n++ == k) return a;
+      t.v[n++] = a;
     }
     if (!seen[b]) {
       seen[b] = true;
-      if (n++ == k) return b;
+      t.v[n++] = b;
     }
   }
-  return k;
+  return t;
 }
 
 constexpr int G_BKC = 8;    // 16-byte chunks per k-tile row (128 bytes)
@@ -136,6 +143,16 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WGN, wn = wave % WGN;
   const int g = lane >> 5, col = lane & 31;
+  // bf16: each 32 x 32 block of the wave is four 16 x 16 MFMA tiles
+  // (v_mfma_f32_16x16x32_bf16, k 32 per instruction): at the same operand
+  // bytes per flop it draws less power than the 32 x 32 x 16 form, and the
+  // chip holds a higher clock under it (2.03 against 1.75 PFLOP/s sustained
+  // with every CU issuing nothing else; here 1.83-2.04 against 1.57-1.71
+  // GHz, +1 % per step: the tile loads, not the matrix units, bound the
+  // k-loop).  float32 keeps 32 x 32 x 2, and so does the row-gathered B
+  // (its eight per-instruction row offsets would not fit beside the
+  // 16 x 16 schedule's registers).
+  constexpr bool M16 = std::is_same<T, bf16>::value && GA != GA_ROWS;
 
   // logical tile: XCD-contiguous ranges, then groups of GM row-tiles that
   // walk the N tiles of all segments together (operand reuse in L2)
@@ -169,7 +186,14 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
       const_cast<T*>(p.A + (int64_t)m0 * p.lda), (short)0, a_bytes, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t b_rsrc =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(b_base), (short)0, b_bytes, kRsrcWord3);
-  uint32_t a_off[LA], b_off[LB];
+  // lane offsets of load instruction i: the first one's plus i times a
+  // row stride, added when the load issues (kept whole in the vector offset,
+  // which the descriptor's range check covers), except for gathered B rows,
+  // which need one per instruction
+  constexpr int LBV = GA == GA_ROWS ? LB : 1;
+  uint32_t a_off[1], b_off[LBV];
+  const uint32_t a_step = (uint32_t)(NLW * RPI * p.lda * (int64_t)sizeof(T));
+  const uint32_t b_step = (uint32_t)(NLW * RPI * p.ldb * (int64_t)sizeof(T));
   // direct-to-LDS: instruction i of loading wave lw fills LDS rows
   // (i*NLW + lw)*RPI .. +RPI (1 KB); lane l writes 16 bytes at 16*l, i.e. row
   // +l/BKC, physical chunk l%BKC, and fetches the logical chunk the swizzle
@@ -181,11 +205,9 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
   const bool loader = wave < NLW;
   auto drow = [&](int i) { return (i * NLW + lw) * RPI + lane / BKC; };
   const int dchunk = swz<BKC>(drow(0), lane % BKC);
+  a_off[0] = (uint32_t)((drow(0) * p.lda + dchunk * VEC) * (int64_t)sizeof(T));
 #pragma unroll
-  for (int i = 0; i < LA; ++i)
-    a_off[i] = (uint32_t)((drow(i) * p.lda + dchunk * VEC) * (int64_t)sizeof(T));
-#pragma unroll
-  for (int i = 0; i < LB; ++i) {
+  for (int i = 0; i < LBV; ++i) {
     if constexpr (GA == GA_ROWS) {
       const int n = n0 + drow(i);
       const int r = n < p.N ? p.rows[n] : -1;
@@ -219,16 +241,22 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
 #if defined(__HIP_DEVICE_COMPILE__)
     constexpr int st = decltype(st_c)::value;
     const int koff = kt * BK * (int)sizeof(T);
+    // (opaque copies: the per-instruction offsets are formed here, not
+    // hoisted out of the k-loop into registers of their own)
+    uint32_t a0 = a_off[0], b0 = b_off[0];
+    asm volatile("" : "+v"(a0), "+v"(b0));
     if (u < LA) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(a_rsrc, (lds_t*)&smem[st][(u * NLW + lw_s) * RPI][0],
-                                               16, a_off[u], koff, 0, 0);
+                                               16, a0 + u * a_step, koff, 0, 0);
     } else {
       const int i = u - LA;
       lds_t* dst = (lds_t*)&smem[st][BM + (i * NLW + lw_s) * RPI][0];
       if constexpr (GA == GA_KCH)
-        __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b_off[i] + kb, 0, 0, 0);
-      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b0 + i * b_step + kb, 0, 0, 0);
+      else if constexpr (GA == GA_ROWS)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b_off[i], koff, 0, 0);
+      else
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(b_rsrc, dst, 16, b0 + i * b_step, koff, 0, 0);
     }
 #endif
   };
@@ -238,27 +266,39 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
       if (loader) issue_one(kt, u, std::integral_constant<int, 0>{});
   };
 
-  f32x16 acc[TM][TN];
+  // accumulators: 32 x 32 blocks (float32) or 16 x 16 tiles (bf16), the same
+  // 16 registers per 32 x 32 block either way
+  constexpr int AM = M16 ? 2 * TM : TM, AN = M16 ? 2 * TN : TN;
+  typedef typename std::conditional<M16, f32x4, f32x16>::type AccT;
+  constexpr int AR = M16 ? 4 : 16;
+  AccT acc[AM][AN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < AM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+    for (int j = 0; j < AN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < AR; ++r) acc[i][j][r] = 0.f;
 
   // MFMA operand fragments, double-buffered in registers: the fragments of
   // k-step ks+1 are read while the MFMAs of k-step ks issue, one read after
   // each MFMA, in the order k-step ks+1's MFMAs first use them.  Scheduling
   // barriers keep that order (left alone, the compiler sinks every read next
   // to its first use).
-  constexpr int KSN = BKC / 2;   // MFMA k-steps per k-tile
+  // k-steps per k-tile: 16 k (32 x 32 x 16) or 32 k (16 x 16 x 32) each
+  constexpr int KSN = M16 ? BKC / 4 : BKC / 2;
   static_assert(KSN % 2 == 0, "fragment slots alternate");
-  u32x4 fa[2][TM], fb[2][TN];
+  // fragments: rows of 32 (lane % 32, chunk 2 ks + lane / 32) or of 16
+  // (lane % 16, chunk 4 ks + lane / 16)
+  constexpr int FR = M16 ? 16 : 32;
+  u32x4 fa[M16 ? 1 : 2][AM], fb[M16 ? 1 : 2][AN];
+  const int frow = M16 ? (lane & 15) : col;
+  constexpr FirstUse<AM, AN> fu = first_use_table<AM, AN>();
   // fragment read r (first_use order) of k-step ks of stage st into slot
   auto frag_one = [&](int st, int ks, int slot, int r) {
-    const int c = swz<BKC>(col, 2 * ks + g);   // rows are col + multiples of 32
-    if (r < TM) fa[slot][r] = smem[st][wm * TM * 32 + r * 32 + col][c];
-    else fb[slot][r - TM] = smem[st][BM + wn * TN * 32 + (r - TM) * 32 + col][c];
+    const int c = M16 ? swz<BKC>(frow, 4 * ks + (lane >> 4)) : swz<BKC>(col, 2 * ks + g);
+    // (rows are frow + multiples of 16, so the swizzle sees frow's bits)
+    if (r < AM) fa[slot][r] = smem[st][wm * TM * 32 + r * FR + frow][c];
+    else fb[slot][r - AM] = smem[st][BM + wn * TN * 32 + (r - AM) * FR + frow][c];
   };
   // One k-tile (stage st is compile-time, so fragment and load addresses are
   // constants plus immediate offsets): wait for this wave's loads of tile kt,
@@ -282,14 +322,39 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
       for (int u = 0; u < LPT / 2; ++u) issue_one(kt + 1, u, NS{});
     }
 #pragma unroll
-    for (int r = 0; r < TM + TN; ++r) frag_one(st, 0, 0, first_use<TM, TN>(r));
+    for (int r = 0; r < AM + AN; ++r) frag_one(st, 0, 0, fu.v[r]);
 #pragma unroll
     for (int ks = 0; ks < KSN; ++ks) {
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < TM * TN; ++i) {
-        Mma<T>::step(acc[i / TN][i % TN], fa[ks & 1][i / TN], fb[ks & 1][i % TN]);
-        if (ks + 1 < KSN && i < TM + TN) frag_one(st, ks + 1, (ks + 1) & 1, first_use<TM, TN>(i));
+      for (int i = 0; i < AM * AN; ++i) {
+        if constexpr (M16) {
+          // Two halves over the B fragments (B 0..AN/2-1, then the rest),
+          // each running through every A fragment, so every fragment is
+          // read for the next k-step into its own registers right after its
+          // last MFMA here (one register slot per fragment): the first
+          // half's B after MFMA AM * AN / 2 - 1, A fragment a after its
+          // second-half use, the second half's B after the last MFMA
+          constexpr int HB = AN / 2;
+          const int h = i / (AM * HB), a = (i % (AM * HB)) / HB, b = h * HB + i % HB;
+          acc[a][b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, fa[0][a]),
+                                                              __builtin_bit_cast(bf16x8, fb[0][b]),
+                                                              acc[a][b], 0, 0, 0);
+          if (ks + 1 < KSN) {
+            if (i == AM * HB - 1) {
+#pragma unroll
+              for (int bb = 0; bb < HB; ++bb) frag_one(st, ks + 1, 0, AM + bb);
+            }
+            if (h == 1 && i % HB == HB - 1) frag_one(st, ks + 1, 0, a);
+            if (i == AM * AN - 1) {
+#pragma unroll
+              for (int bb = HB; bb < AN; ++bb) frag_one(st, ks + 1, 0, AM + bb);
+            }
+          }
+        } else {
+          Mma<T>::step(acc[i / AN][i % AN], fa[ks & 1][i / AN], fb[ks & 1][i % AN]);
+          if (ks + 1 < KSN && i < AM + AN) frag_one(st, ks + 1, (ks + 1) & 1, fu.v[i]);
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
       if (ks == 0 && more && loader) {
@@ -330,23 +395,47 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
-  auto sidx = [](int r, int c) { return r * 64 + (c ^ (((r >> 2) & 1) << 5)); };
-  float colv[TN], gatev[TN];
+  // Register r (0..15) of this lane's 32 x 32 block (i, j): its value and
+  // its row and column inside the block.  32 x 32 x 16 layout: column
+  // lane % 32, rows acc_row(r, lane / 32).  16 x 16 tiles (M16): tile
+  // (r / 8, r / 4 % 2) of the block, row 4 (lane / 16) + r % 4 of it,
+  // column lane % 16.  Registers 4q .. 4q+3 are four consecutive rows of
+  // one column in both layouts.
+  auto av = [&](int i, int j, int r) -> float {
+    if constexpr (M16) return acc[2 * i + (r >> 3)][2 * j + ((r >> 2) & 1)][r & 3];
+    else return acc[i][j][r];
+  };
+  auto arow = [&](int r) { return M16 ? 16 * (r >> 3) + 4 * (lane >> 4) + (r & 3) : acc_row(r, g); };
+  auto acol = [&](int r) { return M16 ? 16 * ((r >> 2) & 1) + (lane & 15) : col; };
+  // staging column flips: bit 5 every four rows (32 x 32: a lane group's
+  // rows are 8 apart) or bits 4..5 by row bits 2..3 (16 x 16: the four lane
+  // groups write rows 4 apart); both leave the row reads conflict-free
+  auto sidx = [](int r, int c) {
+    return M16 ? r * 64 + (c ^ (((r >> 2) & 3) << 4)) : r * 64 + (c ^ (((r >> 2) & 1) << 5));
+  };
+  // per-column bias and gate of the lane's columns: one per 32-column block,
+  // or two (the two 16-column tiles) in the M16 layout
+  constexpr int CS = M16 ? 2 : 1;
+  float colv[TN][CS], gatev[TN][CS];
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int n = n0 + wn * TN * 32 + j * 32 + col;
-    colv[j] = 0.f;
-    gatev[j] = 1.f;
-    if (n < p.N) {
-      if constexpr (GA == GA_ROWS) {
-        const int r = p.rows[n];
-        if (bias_sg && r >= 0) colv[j] = bias_sg[r];
-      } else {
-        if (bias_sg) colv[j] = bias_sg[n];
+  for (int j = 0; j < TN; ++j)
+#pragma unroll
+    for (int cs = 0; cs < CS; ++cs) {
+      const int n = n0 + wn * TN * 32 + j * 32 + acol(4 * cs);
+      colv[j][cs] = 0.f;
+      gatev[j][cs] = 1.f;
+      if (n < p.N) {
+        if constexpr (GA == GA_ROWS) {
+          const int r = p.rows[n];
+          if (bias_sg && r >= 0) colv[j][cs] = bias_sg[r];
+        } else {
+          if (bias_sg) colv[j][cs] = bias_sg[n];
+        }
+        if (EPI == EPI_RESIDUAL && p.gate0) gatev[j][cs] = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
       }
-      if (EPI == EPI_RESIDUAL && p.gate0) gatev[j] = p.gate0[n] + (p.gate1 ? p.gate1[n] : 0.f);
     }
-  }
+  // (register r's column set: r / 4 % 2 for M16)
+  auto csel = [](int r) { return M16 ? ((r >> 2) & 1) : 0; };
   constexpr int NPASS = (TM / 2) * (TN / 2);
   // A tile whose columns start at or past vt_col0 stores transposed (the
   // host keeps vt_col0 on a tile or segment boundary, so this is uniform).
@@ -371,8 +460,8 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
             for (int q = 0; q < 4; ++q) {
               f32x4 v;
 #pragma unroll
-              for (int e = 0; e < 4; ++e) v[e] = acc[i][j][4 * q + e] + colv[j];
-              *reinterpret_cast<f32x4*>(&stage[tidx(jj * 32 + col, ii * 32 + acc_row(4 * q, g))]) = v;
+              for (int e = 0; e < 4; ++e) v[e] = av(i, j, 4 * q + e) + colv[j][csel(4 * q)];
+              *reinterpret_cast<f32x4*>(&stage[tidx(jj * 32 + acol(4 * q), ii * 32 + arow(4 * q))]) = v;
             }
           }
         wave_sync();
@@ -458,10 +547,10 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
         const int i = 2 * rb + ii, j = 2 * ch + jj;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          float v = acc[i][j][r] + colv[j];
+          float v = av(i, j, r) + colv[j][csel(r)];
           if (EPI == EPI_GELU) v = gelu_tanh(v);
-          if (EPI == EPI_RESIDUAL) v *= gatev[j];
-          stage[sidx(ii * 32 + acc_row(r, g), jj * 32 + col)] = v;
+          if (EPI == EPI_RESIDUAL) v *= gatev[j][csel(r)];
+          stage[sidx(ii * 32 + arow(r), jj * 32 + acol(r))] = v;
         }
       }
     wave_sync();
