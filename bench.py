@@ -402,35 +402,37 @@ def gemm_vs_library(args, cfg):
 
 
 def mfma_ceiling(args):
-    """The sustained rate of the bf16 MFMA all the kernels use, with every CU
-    busy and nothing else running (the chip's power limit sets the clock):
-    the ceiling against which the kernels' fraction of the 2.5 PFLOP/s
-    nominal peak is read."""
+    """The sustained rate of each bf16 MFMA shape the kernels use, with every
+    CU busy and nothing else running (the chip's power limit sets the clock,
+    and the shape changes it): the ceilings against which the kernels'
+    fractions of the 2.5 PFLOP/s nominal peak are read."""
     import torch
 
     from paper_2607_06631_amd import binding as B
 
     sink = torch.zeros(1, device="cuda", dtype=torch.float32)
     iters = 300000   # about 0.1 s per launch
-    for _ in range(max(args.warmup, 1)):
-        B.dif_mfma_probe(iters, sink)
-    torch.cuda.synchronize()
-    rates = []
-    for _ in range(max(args.steps, 3)):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        fl = B.dif_mfma_probe(iters, sink)
-        e1.record()
+    out = {}
+    for shape, name in ((B.MFMA_32X32X16, "32x32x16"), (B.MFMA_16X16X32, "16x16x32")):
+        for _ in range(max(args.warmup, 1)):
+            B.dif_mfma_probe(iters, sink, shape)
         torch.cuda.synchronize()
-        rates.append(fl / e0.elapsed_time(e1) / 1e9)
-    rates.sort()
-    med = rates[len(rates) // 2]
-    print(json.dumps({"metric": "sustained bf16 MFMA rate (v_mfma_f32_32x32x16_bf16, all CUs, "
-                                "no memory traffic)",
-                      "tflops_median": round(med, 1), "tflops_min": round(rates[0], 1),
-                      "tflops_max": round(rates[-1], 1),
-                      "frac_nominal_peak": round(med / PEAK_BF16_TFLOPS, 4),
-                      "launches": len(rates), "flop_per_launch": fl}))
+        rates = []
+        for _ in range(max(args.steps, 3)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fl = B.dif_mfma_probe(iters, sink, shape)
+            e1.record()
+            torch.cuda.synchronize()
+            rates.append(fl / e0.elapsed_time(e1) / 1e9)
+        rates.sort()
+        med = rates[len(rates) // 2]
+        out[name] = {"tflops_median": round(med, 1), "tflops_min": round(rates[0], 1),
+                     "tflops_max": round(rates[-1], 1),
+                     "frac_nominal_peak": round(med / PEAK_BF16_TFLOPS, 4),
+                     "launches": len(rates), "flop_per_launch": fl}
+    print(json.dumps({"metric": "sustained bf16 MFMA rate per instruction shape (all CUs, no "
+                                "memory traffic)", "shapes": out}))
 
 
 def main():

@@ -445,18 +445,20 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
 
 /* The matrix cores' sustained rate, for the roofline's context: launches
  * (on `stream`, asynchronously) a kernel that keeps every CU's matrix units
- * issuing v_mfma_f32_32x32x16_bf16 -- the instruction every MFMA kernel of
- * this library uses -- on random operands, `iters` x 8 MFMAs per wave
- * (iters rounded up to a multiple of 4; 300000 take about 0.1 s), two
- * workgroups of four waves per CU, with no memory traffic, and sets *flops
- * to the FLOPs it performs.  Time it with events on the same stream:
+ * issuing one bf16 MFMA shape -- `shape` 0: v_mfma_f32_32x32x16_bf16 (the
+ * attention kernels'), 1: v_mfma_f32_16x16x32_bf16 (the bf16 GEMM's) -- on
+ * random operands, `iters` x 262144 FLOPs per wave (8 or 16 MFMAs; iters
+ * rounded up to a multiple of 4; 300000 take about 0.1 s), two workgroups
+ * of four waves per CU, with no memory traffic, and sets *flops to the FLOPs
+ * it performs.  Time it with events on the same stream:
  * FLOPs / time is the rate the chip holds under its power limit with
  * nothing but MFMAs to do.  `sink` is a device float the kernel may write
  * (it never does for any realistic result; it keeps the work from being
- * optimised away).  Errors: DIF_E_ARG for iters outside 1 .. 10^7 (a
- * launch of a few seconds at most) or a null pointer, DIF_E_UNSUPPORTED off
- * gfx950. */
-dif_status dif_mfma_probe(int32_t iters, float* sink, double* flops, dif_stream stream);
+ * optimised away).  Errors: DIF_E_ARG for a shape other than 0 or 1, iters
+ * outside 1 .. 10^7 (a launch of a few seconds at most) or a null pointer,
+ * DIF_E_UNSUPPORTED off gfx950. */
+dif_status dif_mfma_probe(int32_t shape, int32_t iters, float* sink, double* flops,
+                          dif_stream stream);
 
 /* ------------------------------------------------------------------------
  * Kernel timing: while enabled, every kernel the library launches is

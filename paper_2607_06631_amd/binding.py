@@ -114,7 +114,7 @@ def lib():
                                        i32, i32, vp, sz, vp]),
             "dif_attention_ex_static": (i32, [i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, i64, i32,
                                               i32, i32, i32, vp]),
-            "dif_mfma_probe": (i32, [i32, vp, C.POINTER(C.c_double), vp]),
+            "dif_mfma_probe": (i32, [i32, i32, vp, C.POINTER(C.c_double), vp]),
             "dif_profile_enable": (i32, [i32]),
             "dif_profile_reset": (i32, []),
             "dif_profile_kind_name": (C.c_char_p, [i32]),
@@ -470,11 +470,15 @@ def dif_attention(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim:
 DIF_ATTN_Q_PRESCALED = 1
 
 
-def dif_mfma_probe(iters: int, sink, stream=None) -> float:
-    """Launches the sustained-MFMA-rate kernel; returns its FLOPs (time it
-    with events on the same stream).  `sink`: a float32 device tensor."""
+MFMA_32X32X16, MFMA_16X16X32 = 0, 1
+
+
+def dif_mfma_probe(iters: int, sink, shape: int = MFMA_32X32X16, stream=None) -> float:
+    """Launches the sustained-MFMA-rate kernel for one bf16 MFMA shape;
+    returns its FLOPs (time it with events on the same stream).  `sink`: a
+    float32 device tensor."""
     fl = C.c_double()
-    _check(lib().dif_mfma_probe(iters, sink.data_ptr(), C.byref(fl), _stream(stream)))
+    _check(lib().dif_mfma_probe(shape, iters, sink.data_ptr(), C.byref(fl), _stream(stream)))
     return fl.value
 
 

@@ -1391,15 +1391,17 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
   GUARD_END
 }
 
-dif_status dif_mfma_probe(int32_t iters, float* sink, double* flops, dif_stream stream) {
+dif_status dif_mfma_probe(int32_t shape, int32_t iters, float* sink, double* flops,
+                          dif_stream stream) {
   GUARD_BEGIN
+  if (shape != 0 && shape != 1) return fail(DIF_E_ARG, "shape %d is not 0 or 1", shape);
   if (iters < 1 || iters > 10000000) return fail(DIF_E_ARG, "iters %d outside 1 .. 10^7", iters);
   if (!sink || !flops) return fail(DIF_E_ARG, "null argument");
   if (!is_gfx950()) return fail(DIF_E_UNSUPPORTED, "current HIP device is not gfx950");
   int dev = 0, ncu = 0;
   HIP_TRY(hipGetDevice(&dev));
   HIP_TRY(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev));
-  HIP_TRY(dif::launch_mfma_probe(iters, sink, ncu, static_cast<hipStream_t>(stream), flops));
+  HIP_TRY(dif::launch_mfma_probe(shape, iters, sink, ncu, static_cast<hipStream_t>(stream), flops));
   return DIF_OK;
   GUARD_END
 }

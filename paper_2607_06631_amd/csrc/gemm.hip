@@ -4,7 +4,8 @@
 // per-lane layout the MFMA operands want: every lane feeds a 16-byte run of
 // consecutive k. Workgroup tile 256 x 256 (128 x 128 for small problems),
 // k-tile 128 bytes per row (64 bf16 / 32 f32), split over a grid of waves
-// that each own a block of MFMA 32x32 tiles. Operand tiles are copied
+// that each own a block of 32x32 output blocks (bf16: four 16x16x32 MFMA
+// tiles each; f32: one 32x32x2 tile). Operand tiles are copied
 // global -> LDS by buffer loads that write LDS directly (no staging
 // registers, no LDS store instructions), double-buffered (2 x 64 KB of the
 // 160 KB LDS at 256 x 256): tile kt+1 is requested while tile kt is
@@ -117,8 +118,8 @@ __device__ __forceinline__ void store4(float* p, const float* v) {
   *reinterpret_cast<f32x4*>(p) = x;
 }
 
-// WGM x WGN waves; each wave owns TM x TN MFMA 32x32 tiles; two LDS stages of
-// BKC 16-byte chunks per operand row.
+// WGM x WGN waves; each wave owns TM x TN 32x32 output blocks; two LDS stages
+// of BKC 16-byte chunks per operand row.
 template <typename T, typename OutT, int EPI, int GA, int WGM, int WGN, int TM, int TN, int BKC>
 __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kernel(GemmParams<T, OutT> p) {
   constexpr int NW = WGM * WGN;
@@ -692,13 +693,16 @@ hipError_t launch_gemm(const T* A, int64_t lda, const T* B, int64_t ldb, OutT* C
 }
 
 // The chip's sustained MFMA rate with nothing else running: every CU holds
-// two workgroups of four waves, each wave issuing independent
-// v_mfma_f32_32x32x16_bf16 on eight accumulators (operands from a hash of
-// the thread: random-looking bf16 of magnitude ~1, rotated between
-// iterations), no memory traffic.  The result only decides whether a
-// never-taken store happens, so the work cannot be optimised away.  The
-// rate it reaches is the ceiling the power limit leaves for MFMA-bound
-// kernels (the clock drops below its 2.4 GHz maximum under this load).
+// two workgroups of four waves, each wave issuing independent bf16 MFMAs
+// (32 x 32 x 16 on eight accumulators, or 16 x 16 x 32 on sixteen, the
+// same FLOPs per iteration) on operands from a hash of the thread
+// (random-looking bf16 of magnitude ~1, rotated between iterations), no
+// memory traffic.  The result only decides whether a never-taken store
+// happens, so the work cannot be optimised away.  The rate it reaches is
+// the ceiling the power limit leaves for MFMA-bound kernels of that shape
+// (the clock drops below its 2.4 GHz maximum under this load, and by how
+// much depends on the shape).
+template <bool M16>
 __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters4, float* sink) {
   const uint32_t t = blockIdx.x * 256u + threadIdx.x;
   bf16x8 a[4], b[4];
@@ -713,31 +717,42 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters4, float* s
       a[i][e] = (bf16)(((float)(h & 0xffff) - 32768.f) / 32768.f);
       b[i][e] = (bf16)(((float)(h >> 16) - 32768.f) / 32768.f);
     }
-  f32x16 c[8];
+  typedef typename std::conditional<M16, f32x4, f32x16>::type AccT;
+  constexpr int NACC = M16 ? 16 : 8, NR = M16 ? 4 : 16;   // 262144 FLOPs per u step either way
+  AccT c[NACC];
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int j = 0; j < NACC; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) c[j][r] = 0.f;
+    for (int r = 0; r < NR; ++r) c[j][r] = 0.f;
   for (int it = 0; it < iters4; ++it) {
 #pragma unroll
     for (int u = 0; u < 4; ++u)
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(j + u) & 3], b[j & 3], c[j], 0, 0, 0);
+      for (int j = 0; j < NACC; ++j) {
+        if constexpr (M16)
+          c[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[(j + u) & 3], b[(j >> 2) & 3], c[j], 0, 0, 0);
+        else
+          c[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[(j + u) & 3], b[j & 3], c[j], 0, 0, 0);
+      }
   }
   float sum = 0.f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j)
+  for (int j = 0; j < NACC; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sum += c[j][r];
+    for (int r = 0; r < NR; ++r) sum += c[j][r];
   if (sum == 1234567.f) *sink = sum;
 }
 
-hipError_t launch_mfma_probe(int iters, float* sink, int ncu, hipStream_t stream, double* flops) {
+hipError_t launch_mfma_probe(int shape, int iters, float* sink, int ncu, hipStream_t stream,
+                             double* flops) {
   const int iters4 = (iters + 3) / 4;
   const int blocks = 2 * ncu;
+  // per wave and iteration: 8 MFMAs of 32 x 32 x 16 or 16 of 16 x 16 x 32
   *flops = (double)blocks * 4 * (4.0 * iters4) * 8 * (2.0 * 32 * 32 * 16);
-  hipLaunchKernelGGL(mfma_probe_kernel, dim3(blocks), dim3(256), 0, stream, iters4, sink);
+  if (shape == 0)
+    hipLaunchKernelGGL(mfma_probe_kernel<false>, dim3(blocks), dim3(256), 0, stream, iters4, sink);
+  else
+    hipLaunchKernelGGL(mfma_probe_kernel<true>, dim3(blocks), dim3(256), 0, stream, iters4, sink);
   return hipGetLastError();
 }
 

@@ -118,8 +118,10 @@ hipError_t launch_gemv(const T* W, const float* x, const float* bias, float* out
                        hipStream_t stream);
 
 hipError_t launch_sinusoid(float t, int dim, float* out, hipStream_t stream);
-// Sustained-MFMA-rate probe: 2 workgroups per CU; *flops = FLOPs of the launch.
-hipError_t launch_mfma_probe(int iters, float* sink, int ncu, hipStream_t stream, double* flops);
+// Sustained-MFMA-rate probe (shape 0: 32x32x16, 1: 16x16x32 bf16): 2
+// workgroups per CU; *flops = FLOPs of the launch.
+hipError_t launch_mfma_probe(int shape, int iters, float* sink, int ncu, hipStream_t stream,
+                             double* flops);
 hipError_t launch_silu(const float* x, float* y, int n, hipStream_t stream);
 hipError_t launch_euler(float* z, const float* v, float dsig, int64_t n, hipStream_t stream);
 

@@ -348,11 +348,13 @@ void operator_cases(Arena& ar) {
   {
     float* sink = static_cast<float*>(ar.get(sizeof(float)));
     double fl = 0;
-    EXPECT(dif_mfma_probe(5, sink, &fl, nullptr) == DIF_OK && fl > 0);
-    EXPECT(dif_mfma_probe(0, sink, &fl, nullptr) == DIF_E_ARG);
-    EXPECT(dif_mfma_probe(10000001, sink, &fl, nullptr) == DIF_E_ARG);
-    EXPECT(dif_mfma_probe(5, nullptr, &fl, nullptr) == DIF_E_ARG);
-    EXPECT(dif_mfma_probe(5, sink, nullptr, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(0, 5, sink, &fl, nullptr) == DIF_OK && fl > 0);
+    EXPECT(dif_mfma_probe(1, 5, sink, &fl, nullptr) == DIF_OK && fl > 0);
+    EXPECT(dif_mfma_probe(2, 5, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(0, 0, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(0, 10000001, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(0, 5, nullptr, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(0, 5, sink, nullptr, nullptr) == DIF_E_ARG);
   }
   // attention: plain and the block's launch (pre-scaled queries, split workspace)
   const int Bn = 1, L = 300, H = 3, dh = 128;

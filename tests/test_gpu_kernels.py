@@ -181,24 +181,27 @@ def test_attention_long_keys_ring_leftovers(Lk):
 
 @pytest.mark.gpu
 def test_mfma_probe_rate_is_plausible():
-    """dif_mfma_probe: FLOPs as documented (iters rounded up to a multiple of
-    4; 2 workgroups x 4 waves per CU x 8 MFMAs of 32x32x16 per iteration),
-    a rate between a tenth and all of the 2.5 PFLOP/s nominal peak, and the
-    guard store never taken; a bad argument is rejected."""
+    """dif_mfma_probe, both MFMA shapes: FLOPs as documented (iters rounded up
+    to a multiple of 4; 2 workgroups x 4 waves per CU x 262144 FLOPs per
+    iteration), a rate between a tenth and all of the 2.5 PFLOP/s nominal
+    peak, and the guard store never taken; bad arguments are rejected."""
     import torch
     say("mfma probe")
     ncu = torch.cuda.get_device_properties(0).multi_processor_count
     sink = torch.zeros(1, device="cuda", dtype=torch.float32)
-    fl = B.dif_mfma_probe(1001, sink)
-    assert fl == 2 * ncu * 4 * 1004 * 8 * 2 * 32 * 32 * 16
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    fl = B.dif_mfma_probe(2000, sink)
-    e1.record()
-    torch.cuda.synchronize()
-    tflops = fl / e0.elapsed_time(e1) / 1e9
-    say(f"  {tflops:.1f} TFLOP/s")
-    assert 250.0 < tflops <= 2500.0
+    for shape in (B.MFMA_32X32X16, B.MFMA_16X16X32):
+        fl = B.dif_mfma_probe(1001, sink, shape)
+        assert fl == 2 * ncu * 4 * 1004 * 8 * 2 * 32 * 32 * 16
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        fl = B.dif_mfma_probe(2000, sink, shape)
+        e1.record()
+        torch.cuda.synchronize()
+        tflops = fl / e0.elapsed_time(e1) / 1e9
+        say(f"  shape {shape}: {tflops:.1f} TFLOP/s")
+        assert 250.0 < tflops <= 2500.0
     assert sink.item() == 0.0
     with pytest.raises(B.DifError):
         B.dif_mfma_probe(0, sink)
+    with pytest.raises(B.DifError):
+        B.dif_mfma_probe(10, sink, 2)
