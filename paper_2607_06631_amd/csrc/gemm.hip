@@ -356,9 +356,17 @@ __global__ __launch_bounds__(64 * WGM * WGN, 8 / (WGM * WGN)) void gemm_nt_kerne
           Mma<T>::step(acc[i / AN][i % AN], fa[ks & 1][i / AN], fb[ks & 1][i % AN]);
           if (ks + 1 < KSN && i < AM + AN) frag_one(st, ks + 1, (ks + 1) & 1, fu.v[i]);
         }
+        // the tile's second half of loads: after the first k-step's MFMAs
+        // (32 x 32 x 16), or after its first eight (16 x 16 x 32: its k-steps
+        // are half as many and the loads want the time to land; after the
+        // whole k-step 3 % slower, all at the barrier 0.8 %)
+        if (M16 && ks == 0 && i == 7 && more && loader) {
+#pragma unroll
+          for (int u = LPT / 2; u < LPT; ++u) issue_one(kt + 1, u, NS{});
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
-      if (ks == 0 && more && loader) {
+      if (!M16 && ks == 0 && more && loader) {
 #pragma unroll
         for (int u = LPT / 2; u < LPT; ++u) issue_one(kt + 1, u, NS{});
       }
