@@ -413,7 +413,8 @@ def mfma_ceiling(args):
     sink = torch.zeros(1, device="cuda", dtype=torch.float32)
     iters = 300000   # about 0.1 s per launch
     out = {}
-    for shape, name in ((B.MFMA_32X32X16, "32x32x16"), (B.MFMA_16X16X32, "16x16x32")):
+    for shape, name in ((B.MFMA_32X32X16, "32x32x16"), (B.MFMA_16X16X32, "16x16x32"),
+                        (B.PROBE_EXP_F32, "exp_f32")):
         for _ in range(max(args.warmup, 1)):
             B.dif_mfma_probe(iters, sink, shape)
         torch.cuda.synchronize()
@@ -427,12 +428,18 @@ def mfma_ceiling(args):
             rates.append(fl / e0.elapsed_time(e1) / 1e9)
         rates.sort()
         med = rates[len(rates) // 2]
+        if shape == B.PROBE_EXP_F32:
+            # rates are then 10^12 exponentials per second
+            out[name] = {"exps_per_s_median": med * 1e12, "exps_per_s_min": rates[0] * 1e12,
+                         "exps_per_s_max": rates[-1] * 1e12, "launches": len(rates),
+                         "exps_per_launch": fl}
+            continue
         out[name] = {"tflops_median": round(med, 1), "tflops_min": round(rates[0], 1),
                      "tflops_max": round(rates[-1], 1),
                      "frac_nominal_peak": round(med / PEAK_BF16_TFLOPS, 4),
                      "launches": len(rates), "flop_per_launch": fl}
-    print(json.dumps({"metric": "sustained bf16 MFMA rate per instruction shape (all CUs, no "
-                                "memory traffic)", "shapes": out}))
+    print(json.dumps({"metric": "sustained bf16 MFMA rate per instruction shape and v_exp_f32 "
+                                "rate (all CUs, no memory traffic)", "shapes": out}))
 
 
 def main():

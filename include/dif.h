@@ -452,11 +452,15 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
  * of four waves per CU, with no memory traffic, and sets *flops to the FLOPs
  * it performs.  Time it with events on the same stream:
  * FLOPs / time is the rate the chip holds under its power limit with
- * nothing but MFMAs to do.  `sink` is a device float the kernel may write
- * (it never does for any realistic result; it keeps the work from being
- * optimised away).  Errors: DIF_E_ARG for a shape other than 0 or 1, iters
- * outside 1 .. 10^7 (a launch of a few seconds at most) or a null pointer,
- * DIF_E_UNSUPPORTED off gfx950. */
+ * nothing but MFMAs to do.  `shape` 2 measures the softmax's exponential
+ * the same way: eight workgroups of four waves per CU, every lane
+ * evaluating `iters` x 16 v_exp_f32 (sixteen independent chains
+ * x <- 2^-x; 300000 take about 0.15 s), and *flops is set to the number of
+ * exponentials.  `sink` is a device float the kernel may
+ * write (it never does for any realistic result; it keeps the work from
+ * being optimised away).  Errors: DIF_E_ARG for a shape other than 0, 1 or
+ * 2, iters outside 1 .. 10^7 (a launch of a few seconds at most) or a null
+ * pointer, DIF_E_UNSUPPORTED off gfx950. */
 dif_status dif_mfma_probe(int32_t shape, int32_t iters, float* sink, double* flops,
                           dif_stream stream);
 

@@ -470,13 +470,14 @@ def dif_attention(Q, K, Vt, O, B: int, Lq: int, Lk: int, n_heads: int, head_dim:
 DIF_ATTN_Q_PRESCALED = 1
 
 
-MFMA_32X32X16, MFMA_16X16X32 = 0, 1
+MFMA_32X32X16, MFMA_16X16X32, PROBE_EXP_F32 = 0, 1, 2
 
 
 def dif_mfma_probe(iters: int, sink, shape: int = MFMA_32X32X16, stream=None) -> float:
-    """Launches the sustained-MFMA-rate kernel for one bf16 MFMA shape;
-    returns its FLOPs (time it with events on the same stream).  `sink`: a
-    float32 device tensor."""
+    """Launches the sustained-rate kernel for one bf16 MFMA shape (or, for
+    PROBE_EXP_F32, the exponential); returns its FLOPs (the exponentials'
+    count for PROBE_EXP_F32; time it with events on the same stream).
+    `sink`: a float32 device tensor."""
     fl = C.c_double()
     _check(lib().dif_mfma_probe(shape, iters, sink.data_ptr(), C.byref(fl), _stream(stream)))
     return fl.value

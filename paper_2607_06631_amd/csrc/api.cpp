@@ -1394,7 +1394,7 @@ dif_status dif_attention_ex_static(int32_t dtype, int32_t head_dim, int32_t flag
 dif_status dif_mfma_probe(int32_t shape, int32_t iters, float* sink, double* flops,
                           dif_stream stream) {
   GUARD_BEGIN
-  if (shape != 0 && shape != 1) return fail(DIF_E_ARG, "shape %d is not 0 or 1", shape);
+  if (shape < 0 || shape > 2) return fail(DIF_E_ARG, "shape %d is not 0, 1 or 2", shape);
   if (iters < 1 || iters > 10000000) return fail(DIF_E_ARG, "iters %d outside 1 .. 10^7", iters);
   if (!sink || !flops) return fail(DIF_E_ARG, "null argument");
   if (!is_gfx950()) return fail(DIF_E_UNSUPPORTED, "current HIP device is not gfx950");

@@ -751,9 +751,38 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int iters4, float* s
   if (sum == 1234567.f) *sink = sum;
 }
 
+// The same for the softmax's exponential (v_exp_f32, the instruction the
+// attention kernels evaluate 2^x with): every lane runs sixteen independent
+// chains x <- 2^(-x), which stay in [0.5, 1] (the negation is a free source
+// modifier, so the loop is nothing but exponentials).  Eight workgroups of
+// four waves per CU (eight waves per SIMD) hide the instruction's latency.
+__global__ __launch_bounds__(256) void exp_probe_kernel(int iters4, float* sink) {
+  const uint32_t t = blockIdx.x * 256u + threadIdx.x;
+  float x[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) x[j] = 0.5f + (float)((t * 16u + (uint32_t)j) & 1023u) / 2048.f;
+  for (int it = 0; it < iters4; ++it) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) x[j] = __builtin_amdgcn_exp2f(-x[j]);
+  }
+  float sum = 0.f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) sum += x[j];
+  if (sum == 1234567.f) *sink = sum;
+}
+
 hipError_t launch_mfma_probe(int shape, int iters, float* sink, int ncu, hipStream_t stream,
                              double* flops) {
   const int iters4 = (iters + 3) / 4;
+  if (shape == 2) {
+    // per lane and iteration: 16 exponentials
+    const int eblocks = 8 * ncu;
+    *flops = (double)eblocks * 256 * (4.0 * iters4) * 16;
+    hipLaunchKernelGGL(exp_probe_kernel, dim3(eblocks), dim3(256), 0, stream, iters4, sink);
+    return hipGetLastError();
+  }
   const int blocks = 2 * ncu;
   // per wave and iteration: 8 MFMAs of 32 x 32 x 16 or 16 of 16 x 16 x 32
   *flops = (double)blocks * 4 * (4.0 * iters4) * 8 * (2.0 * 32 * 32 * 16);

@@ -350,7 +350,9 @@ void operator_cases(Arena& ar) {
     double fl = 0;
     EXPECT(dif_mfma_probe(0, 5, sink, &fl, nullptr) == DIF_OK && fl > 0);
     EXPECT(dif_mfma_probe(1, 5, sink, &fl, nullptr) == DIF_OK && fl > 0);
-    EXPECT(dif_mfma_probe(2, 5, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(2, 5, sink, &fl, nullptr) == DIF_OK && fl > 0);
+    EXPECT(dif_mfma_probe(3, 5, sink, &fl, nullptr) == DIF_E_ARG);
+    EXPECT(dif_mfma_probe(-1, 5, sink, &fl, nullptr) == DIF_E_ARG);
     EXPECT(dif_mfma_probe(0, 0, sink, &fl, nullptr) == DIF_E_ARG);
     EXPECT(dif_mfma_probe(0, 10000001, sink, &fl, nullptr) == DIF_E_ARG);
     EXPECT(dif_mfma_probe(0, 5, nullptr, &fl, nullptr) == DIF_E_ARG);

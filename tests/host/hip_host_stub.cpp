@@ -324,7 +324,7 @@ hipError_t launch_sinusoid(float, int dim, float* out, hipStream_t) {
 
 hipError_t launch_mfma_probe(int shape, int iters, float* sink, int ncu, hipStream_t, double* flops) {
   ++g_stub_launches;
-  check((shape == 0 || shape == 1) && iters >= 1 && ncu >= 1, "mfma_probe: bad launch");
+  check(shape >= 0 && shape <= 2 && iters >= 1 && ncu >= 1, "mfma_probe: bad launch");
   wr(sink, sizeof(float));
   *flops = 2.0 * ncu * 4 * (4.0 * ((iters + 3) / 4)) * 8 * (2.0 * 32 * 32 * 16);
   return hipSuccess;

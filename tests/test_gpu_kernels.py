@@ -181,7 +181,7 @@ def test_attention_long_keys_ring_leftovers(Lk):
 
 @pytest.mark.gpu
 def test_mfma_probe_rate_is_plausible():
-    """dif_mfma_probe, both MFMA shapes: FLOPs as documented (iters rounded up
+    """dif_mfma_probe, both MFMA shapes and the exponential: counts as documented (iters rounded up
     to a multiple of 4; 2 workgroups x 4 waves per CU x 262144 FLOPs per
     iteration), a rate between a tenth and all of the 2.5 PFLOP/s nominal
     peak, and the guard store never taken; bad arguments are rejected."""
@@ -200,8 +200,21 @@ def test_mfma_probe_rate_is_plausible():
         tflops = fl / e0.elapsed_time(e1) / 1e9
         say(f"  shape {shape}: {tflops:.1f} TFLOP/s")
         assert 250.0 < tflops <= 2500.0
+    # the exponential: 8 workgroups x 256 lanes per CU x 16 per iteration,
+    # at a rate above 10^11 per second and no faster than every lane of
+    # every SIMD finishing one per cycle at 2.4 GHz
+    fl = B.dif_mfma_probe(1001, sink, B.PROBE_EXP_F32)
+    assert fl == 8 * ncu * 256 * 1004 * 16
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    fl = B.dif_mfma_probe(20000, sink, B.PROBE_EXP_F32)
+    e1.record()
+    torch.cuda.synchronize()
+    rate = fl / (e0.elapsed_time(e1) * 1e-3)
+    say(f"  exp: {rate:.3e} per second")
+    assert 1e11 < rate <= ncu * 64 * 2.4e9
     assert sink.item() == 0.0
     with pytest.raises(B.DifError):
         B.dif_mfma_probe(0, sink)
     with pytest.raises(B.DifError):
-        B.dif_mfma_probe(10, sink, 2)
+        B.dif_mfma_probe(10, sink, 3)
