@@ -141,7 +141,10 @@ hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0
 // them, with the rotation-table reads in their shadow.
 // ---------------------------------------------------------------------------
 constexpr int QK_WAVES = 8;    // 16 KB of loads in flight per wave; registers for both segments
-constexpr int QK_RPW = 16;
+// rows per wave: 4 gives 32760 video tokens 1024 workgroups, so several share a
+// CU and more rows' loads are in flight (5.1 TB/s; 16 rows per wave, one
+// workgroup per CU, reached 4.9)
+constexpr int QK_RPW = 4;
 template <typename T, int MAXC, int NSEG>
 __global__ __launch_bounds__(64 * QK_WAVES) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
                                                             int nseg, int off0, int off1,
