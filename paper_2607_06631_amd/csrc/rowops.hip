@@ -141,10 +141,12 @@ hipError_t launch_norm(const T* x, T* y, int M, int D, int mode, const float* p0
 // them, with the rotation-table reads in their shadow.
 // ---------------------------------------------------------------------------
 constexpr int QK_WAVES = 8;    // 16 KB of loads in flight per wave; registers for both segments
-// rows per wave: 4 gives 32760 video tokens 1024 workgroups, so several share a
-// CU and more rows' loads are in flight (5.1 TB/s; 16 rows per wave, one
-// workgroup per CU, reached 4.9)
-constexpr int QK_RPW = 4;
+// Rows per wave.  One segment: 4, so 32760 video tokens make 1024 workgroups,
+// several per CU, with more rows' loads in flight (5.3 TB/s; 16 rows per
+// wave, one workgroup per CU, reached 4.2).  Two segments (q and k, twice the
+// loads per row): 16 (5.4-5.5 TB/s against 5.3 with 4).
+template <int NSEG>
+constexpr int qk_rpw() { return NSEG == 2 ? 16 : 4; }
 template <typename T, int MAXC, int NSEG>
 __global__ __launch_bounds__(64 * QK_WAVES) void qk_norm_kernel(T* buf, int64_t ld, int rows, int a,
                                                             int nseg, int off0, int off1,
@@ -163,8 +165,9 @@ __global__ __launch_bounds__(64 * QK_WAVES) void qk_norm_kernel(T* buf, int64_t 
   const int lane = threadIdx.x & 63;
   const int nch = a / VEC;
   const int jb = ((lane * VEC) % rope.head_dim) / 2;  // first head-local pair of this lane
-  for (int rr = 0; rr < QK_RPW; ++rr) {
-    const int64_t row = (int64_t)blockIdx.x * (QK_WAVES * QK_RPW) + (threadIdx.x >> 6) * QK_RPW + rr;
+  constexpr int RPW = qk_rpw<NSEG>();
+  for (int rr = 0; rr < RPW; ++rr) {
+    const int64_t row = (int64_t)blockIdx.x * (QK_WAVES * RPW) + (threadIdx.x >> 6) * RPW + rr;
     if (row >= rows) break;
     // both segments' loads go out before anything waits on them
     u32x4 raw[NSEG][MAXC];
@@ -256,12 +259,13 @@ hipError_t launch_qk_norm(T* buf, int64_t ld, int rows, int a, int nseg, int off
   if (rd.head_dim <= 0) rd.head_dim = 64;   // no rotation: any width dividing 64 * VEC
   constexpr int VEC = Chunk<T>::VEC;
   if ((64 * VEC) % rd.head_dim != 0) return hipErrorInvalidValue;
-  const dim3 grid((rows + QK_WAVES * QK_RPW - 1) / (QK_WAVES * QK_RPW));
   // q and k in one launch while both fit the registers (up to 8 chunks per
   // lane), else one launch per segment
   auto launch = [&](auto c_tag, auto nseg_tag, int off_a, int off_b, const float* ga,
                     const float* gb, float sa) {
     constexpr int C = decltype(c_tag)::value, NS = decltype(nseg_tag)::value;
+    constexpr int rows_per_wg = QK_WAVES * qk_rpw<NS>();
+    const dim3 grid((rows + rows_per_wg - 1) / rows_per_wg);
     hipLaunchKernelGGL((qk_norm_kernel<T, C, NS>), grid, dim3(64 * QK_WAVES), NS * a * sizeof(float),
                        stream, buf, ld, rows, a, NS, off_a, off_b, ga, gb, gain_idx, sa,
                        inv_norm_dim, eps, rd);
